@@ -1,0 +1,314 @@
+"""Pins for the fp64 oracle (CPU only).
+
+Each test ties ``oracle/`` to something other than itself: hand-derived closed
+forms, pure-Python brute force over the un-paged sequence, a library routine
+(torch's causal SDPA in fp64, scipy's logsumexp), closed forms of degenerate
+inputs, and invariants the definition implies (prefix reuse equals recompute,
+paging independence, head-group sharing).  A few tests plant a mistake in the
+oracle's inputs to show the pins have teeth.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+from oracle import brute_force_extend, oracle_append, oracle_extend, storage_to_f64, gather_logical
+from paper_2609_39819_amd.workloads import build_workload, bf16_bits_to_f32
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def _pool_f64_view(w):
+    return w.k_pool_c, w.v_pool_c
+
+
+def _appended(w):
+    """Compact pools after the oracle writes the suffix K/V."""
+    return oracle_append(w.k_pool_c, w.v_pool_c, w.compact_table, w.prefix_len, w.suffix_len, w.k_new, w.v_new)
+
+
+def _oracle(w, **kw):
+    kp, vp = _appended(w)
+    return oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len, w.suffix_len, w.num_kv_heads, w.scale, **kw)
+
+
+def _rel(a, b):
+    return np.max(np.abs(a - b)) / max(1e-300, np.max(np.abs(b)))
+
+
+# ---------------------------------------------------------------------------
+# hand-derived closed forms
+# ---------------------------------------------------------------------------
+
+def _eval(expr):
+    return eval(expr, {"__builtins__": {}}, {"e": math.e, "log": math.log, "exp": math.exp})
+
+
+def test_hand_cases():
+    with open(os.path.join(HERE, "golden", "hand_cases.json")) as f:
+        cases = json.load(f)["cases"]
+    for c in cases:
+        P, S, Hq, Hkv = c["prefix_len"], c["suffix_len"], c["num_q_heads"], c["num_kv_heads"]
+        k = np.array(c["k"], dtype=np.float32)
+        D = k.shape[-1]
+        k = k.reshape(P + S, Hkv, D)
+        v = np.array(c["v"], dtype=np.float32).reshape(P + S, Hkv, D)
+        q = np.array(c["q"], dtype=np.float32).reshape(S, Hq, D)
+        want_out = np.vectorize(_eval, otypes=[float])(np.array(c["out"], dtype=object)).reshape(S, Hq, D)
+        want_lse = np.vectorize(_eval, otypes=[float])(np.array(c["lse"], dtype=object)).reshape(S, Hq)
+        # page it by hand: one block, physical id 3 of a 5-block NaN pool
+        kp = np.full((5, Hkv, 16, D), np.nan, np.float32)
+        vp = np.full((5, Hkv, 16, D), np.nan, np.float32)
+        kp[3, :, :P, :] = k[:P].transpose(1, 0, 2)
+        vp[3, :, :P, :] = v[:P].transpose(1, 0, 2)
+        bt = np.array([[3]], dtype=np.int32)
+        kp, vp = oracle_append(kp, vp, bt, [P], [S], k[P:], v[P:])
+        out, lse = oracle_extend(q, kp, vp, bt, [P], [S], Hkv, c["scale"])
+        assert np.allclose(out, want_out, rtol=1e-14, atol=1e-14), c["name"]
+        assert np.allclose(lse, want_lse, rtol=1e-14, atol=1e-14), c["name"]
+        bo, bl = brute_force_extend(q, [k], [v], [P], [S], Hkv, c["scale"])
+        assert np.allclose(bo, want_out, rtol=1e-14, atol=1e-14), c["name"]
+        assert np.allclose(bl, want_lse, rtol=1e-14, atol=1e-14), c["name"]
+
+
+# ---------------------------------------------------------------------------
+# brute force over the un-paged logical sequence
+# ---------------------------------------------------------------------------
+
+SWEEP = [
+    # (P list, S list, Hq, Hkv, D, dtype)
+    ([p], [s], 4, 1, 8, "bf16") for p in (0, 1, 15, 16, 17, 33) for s in (1, 5, 16, 40)
+] + [
+    ([17, 0, 33], [5, 16, 1], 12, 1, 8, "bf16"),
+    ([16, 15], [40, 3], 4, 4, 8, "f32"),
+    ([33], [16], 12, 1, 64, "bf16"),
+    ([240], [16], 4, 1, 64, "f32"),
+    ([1, 47, 16], [17, 2, 31], 24, 2, 8, "bf16"),
+]
+
+
+@pytest.mark.parametrize("case", range(len(SWEEP)))
+def test_oracle_matches_brute_force(case):
+    P, S, Hq, Hkv, D, dt = SWEEP[case]
+    w = build_workload(name="sweep", seed=100 + case, prefix_len=P, suffix_len=S, num_q_heads=Hq,
+                       num_kv_heads=Hkv, head_dim=D, dtype=dt, num_blocks=64, keep_logical=True)
+    out, lse = _oracle(w)
+    bo, bl = brute_force_extend(w.q, w.logical_k, w.logical_v, w.prefix_len, w.suffix_len, Hkv, w.scale)
+    assert np.all(np.isfinite(out)) and np.all(np.isfinite(lse))
+    assert _rel(out, bo) <= 1e-12
+    assert np.max(np.abs(lse - bl)) <= 1e-12 * max(1.0, np.max(np.abs(bl)))
+
+
+def test_brute_force_catches_planted_mistakes():
+    """Inputs that stand for plausible oracle bugs (mask shifted by one, two
+    pages swapped, wrong head grouping) must fail the brute-force comparison."""
+    w = build_workload(name="mut", seed=7, prefix_len=[33], suffix_len=[20], num_q_heads=8, num_kv_heads=2,
+                       head_dim=8, dtype="bf16", num_blocks=64, keep_logical=True)
+    bo, _ = brute_force_extend(w.q, w.logical_k, w.logical_v, w.prefix_len, w.suffix_len, 2, w.scale)
+    kp, vp = _appended(w)
+    # off-by-one causal window (the diagonal position left out)
+    o1, _ = oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len - 1, w.suffix_len, 2, w.scale)
+    assert _rel(o1, bo) > 1e-3
+    # two pages swapped in the table (one of them straddles the causal edge;
+    # swapping two pages every query sees fully would be invisible, since
+    # attention is a set function of the visible positions)
+    bt = w.compact_table.copy()
+    bt[0, [0, 2]] = bt[0, [2, 0]]
+    o2, _ = oracle_extend(w.q, kp, vp, bt, w.prefix_len, w.suffix_len, 2, w.scale)
+    assert _rel(o2, bo) > 1e-3
+    # interleaved head grouping (h % Hkv instead of h // G)
+    perm = np.array([h // 2 + (h % 2) * 4 for h in range(8)])
+    o3, _ = oracle_extend(w.q[:, perm], kp, vp, w.compact_table, w.prefix_len, w.suffix_len, 2, w.scale)
+    assert _rel(o3[:, np.argsort(perm)], bo) > 1e-3
+
+
+# ---------------------------------------------------------------------------
+# library routines
+# ---------------------------------------------------------------------------
+
+def test_no_prefix_is_textbook_causal_attention():
+    """P = 0 reduces to causal self-attention over the S new tokens: compare
+    with torch's scaled_dot_product_attention(is_causal=True) in fp64."""
+    torch = pytest.importorskip("torch")
+    S, H, D = 37, 3, 16
+    w = build_workload(name="p0", seed=11, prefix_len=[0], suffix_len=[S], num_q_heads=H, num_kv_heads=H,
+                       head_dim=D, dtype="bf16", num_blocks=16, keep_logical=True)
+    out, _ = _oracle(w)
+    q = torch.from_numpy(storage_to_f64(w.q)).permute(1, 0, 2)
+    k = torch.from_numpy(storage_to_f64(w.logical_k[0])).permute(1, 0, 2)
+    v = torch.from_numpy(storage_to_f64(w.logical_v[0])).permute(1, 0, 2)
+    ref = torch.nn.functional.scaled_dot_product_attention(q, k, v, is_causal=True, scale=w.scale)
+    assert _rel(out, ref.permute(1, 0, 2).numpy()) <= 1e-12
+
+
+def test_lse_matches_scipy_logsumexp():
+    sp = pytest.importorskip("scipy.special")
+    w = build_workload(name="lse", seed=12, prefix_len=[50], suffix_len=[9], num_q_heads=4, num_kv_heads=2,
+                       head_dim=32, dtype="bf16", num_blocks=16, keep_logical=True)
+    _, lse = _oracle(w)
+    for i in range(9):
+        for h in range(4):
+            k = storage_to_f64(w.logical_k[0][:50 + i + 1, h // 2])
+            s = w.scale * (k @ storage_to_f64(w.q[i, h]))
+            assert abs(lse[i, h] - sp.logsumexp(s)) <= 1e-12 * max(1, abs(lse[i, h]))
+
+
+# ---------------------------------------------------------------------------
+# closed forms of degenerate inputs
+# ---------------------------------------------------------------------------
+
+def test_zero_keys_average_the_visible_values():
+    """K = 0 makes every logit 0, so each output is the plain mean of V over
+    positions 0..P+i: the divisor P+i+1 pins the causal window length."""
+    P, S = [70, 3], [21, 40]
+    w = build_workload(name="kz", seed=13, prefix_len=P, suffix_len=S, num_q_heads=6, num_kv_heads=2,
+                       head_dim=16, dtype="bf16", num_blocks=64, variant="kzero", keep_logical=True)
+    out, lse = _oracle(w)
+    off = w.seq_offsets
+    for b in range(2):
+        v = storage_to_f64(w.logical_v[b])                      # [L, Hkv, D]
+        csum = np.cumsum(v, axis=0)
+        for i in range(S[b]):
+            n = P[b] + i + 1
+            mean = csum[n - 1] / n                               # [Hkv, D]
+            want = np.repeat(mean, 3, axis=0)
+            assert np.allclose(out[off[b] + i], want, rtol=1e-12, atol=1e-12)
+            assert np.allclose(lse[off[b] + i], math.log(n), rtol=0, atol=1e-12)
+
+
+def test_constant_values_reproduce_the_constant():
+    w = build_workload(name="vc", seed=14, prefix_len=[100], suffix_len=[30], num_q_heads=8, num_kv_heads=4,
+                       head_dim=32, dtype="bf16", num_blocks=64, variant="vconst")
+    out, _ = _oracle(w)
+    c = storage_to_f64(w.extra["vconst"])                         # [Hkv, D]
+    want = np.repeat(c, 2, axis=0)[None]
+    assert np.allclose(out, want, rtol=1e-13, atol=1e-13)
+
+
+def test_needle_selects_its_target_value():
+    """q = 2 K[t] puts logit ~ 2 sqrt(D) on position t, far above the others,
+    so the output is V[t] up to the small residual mass (bounded here by 1e-2)."""
+    w = build_workload(name="nd", seed=15, prefix_len=[2000], suffix_len=[8], num_q_heads=4, num_kv_heads=1,
+                       head_dim=128, dtype="bf16", num_blocks=256, variant="needle", keep_logical=True)
+    out, _ = _oracle(w)
+    tgt = w.extra["needle_target"]
+    v = storage_to_f64(w.logical_v[0])
+    want = v[tgt, 0, :]                                          # [T, Hq, D]
+    assert np.max(np.abs(out - want)) < 1e-2
+
+
+# ---------------------------------------------------------------------------
+# invariants
+# ---------------------------------------------------------------------------
+
+def test_gqa_equals_mha_with_repeated_kv_heads():
+    w = build_workload(name="gqa", seed=16, prefix_len=[45, 9], suffix_len=[12, 30], num_q_heads=12,
+                       num_kv_heads=3, head_dim=16, dtype="bf16", num_blocks=32)
+    out, lse = _oracle(w)
+    kp, vp = _appended(w)
+    kr = np.repeat(kp, 4, axis=1)        # kv-head g copied to heads 4g..4g+3
+    vr = np.repeat(vp, 4, axis=1)
+    o2, l2 = oracle_extend(w.q, kr, vr, w.compact_table, w.prefix_len, w.suffix_len, 12, w.scale)
+    assert _rel(o2, out) <= 1e-13 and np.max(np.abs(l2 - lse)) <= 1e-13
+
+
+def test_paging_is_invisible():
+    """Relabelling physical pages (moving blocks and rewriting the table
+    consistently) leaves the result bit-identical."""
+    w = build_workload(name="perm", seed=17, prefix_len=[77, 160], suffix_len=[19, 4], num_q_heads=4,
+                       num_kv_heads=2, head_dim=16, dtype="bf16", num_blocks=64)
+    out, lse = _oracle(w)
+    kp, vp = _appended(w)
+    rng = np.random.default_rng(0)
+    n = kp.shape[0]
+    perm = rng.permutation(n)              # new position of old block i is perm[i]
+    kq = np.empty_like(kp); vq = np.empty_like(vp)
+    kq[perm] = kp; vq[perm] = vp
+    bt = np.where(w.compact_table >= 0, perm[np.maximum(w.compact_table, 0)], -1).astype(np.int32)
+    o2, l2 = oracle_extend(w.q, kq, vq, bt, w.prefix_len, w.suffix_len, 2, w.scale)
+    assert np.array_equal(o2, out) and np.array_equal(l2, lse)
+
+
+def test_prefix_reuse_equals_full_recompute():
+    """Reusing P cached positions and extending by S gives the same rows as
+    prefilling all P+S positions from scratch (the premise of KV reuse, §1)."""
+    P, S = 53, 27
+    full = build_workload(name="full", seed=18, prefix_len=[0], suffix_len=[P + S], num_q_heads=6,
+                          num_kv_heads=2, head_dim=16, dtype="bf16", num_blocks=16, keep_logical=True)
+    o_full, l_full = _oracle(full)
+    # same logical data, now with the first P positions treated as a reused prefix
+    kp = np.full_like(full.k_pool_c, 0); vp = np.full_like(full.v_pool_c, 0)
+    kp[...] = full.k_pool_c; vp[...] = full.v_pool_c
+    kp, vp = oracle_append(kp, vp, full.compact_table, [0], [P], full.k_new[:P], full.v_new[:P])
+    kp, vp = oracle_append(kp, vp, full.compact_table, [P], [S], full.k_new[P:], full.v_new[P:])
+    o_ext, l_ext = oracle_extend(full.q[P:], kp, vp, full.compact_table, [P], [S], 2, full.scale)
+    assert _rel(o_ext, o_full[P:]) <= 1e-13
+    assert np.max(np.abs(l_ext - l_full[P:])) <= 1e-13
+
+
+def test_chunked_turns_equal_one_turn():
+    """append+extend(P, S1) then append+extend(P+S1, S2) equals append+extend(P, S1+S2)."""
+    P, S1, S2 = 40, 13, 22
+    w = build_workload(name="chunk", seed=19, prefix_len=[P], suffix_len=[S1 + S2], num_q_heads=4,
+                       num_kv_heads=1, head_dim=16, dtype="bf16", num_blocks=16)
+    o_one, _ = _oracle(w)
+    kp, vp = oracle_append(w.k_pool_c, w.v_pool_c, w.compact_table, [P], [S1], w.k_new[:S1], w.v_new[:S1])
+    o_a, _ = oracle_extend(w.q[:S1], kp, vp, w.compact_table, [P], [S1], 1, w.scale)
+    kp, vp = oracle_append(kp, vp, w.compact_table, [P + S1], [S2], w.k_new[S1:], w.v_new[S1:])
+    o_b, _ = oracle_extend(w.q[S1:], kp, vp, w.compact_table, [P + S1], [S2], 1, w.scale)
+    assert _rel(np.concatenate([o_a, o_b]), o_one) <= 1e-13
+
+
+def test_shift_of_all_keys_moves_only_lse():
+    """Adding one vector u to every key adds scale*<q,u> to every logit of a
+    row: the output is unchanged and lse moves by exactly that amount."""
+    w = build_workload(name="shift", seed=20, prefix_len=[31], suffix_len=[6], num_q_heads=2, num_kv_heads=1,
+                       head_dim=8, dtype="f32", num_blocks=8)
+    out, lse = _oracle(w)
+    kp, vp = _appended(w)
+    u = np.linspace(-1, 1, 8)
+    ks = storage_to_f64(kp) + u
+    o2, l2 = oracle_extend(w.q, ks, vp, w.compact_table, w.prefix_len, w.suffix_len, 1, w.scale)
+    assert _rel(o2, out) <= 1e-12
+    want = lse + w.scale * (storage_to_f64(w.q) @ u)
+    assert np.allclose(l2, want, rtol=0, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# append
+# ---------------------------------------------------------------------------
+
+def test_append_places_every_token_and_touches_nothing_else():
+    P, S = [0, 17, 40, 64], [5, 31, 24, 1]
+    w = build_workload(name="app", seed=21, prefix_len=P, suffix_len=S, num_q_heads=2, num_kv_heads=2,
+                       head_dim=8, dtype="bf16", num_blocks=40, keep_logical=True)
+    kp, vp = _appended(w)
+    touched = np.zeros(kp.shape[:3], dtype=bool)          # [block, head, slot]
+    for b in range(4):
+        L = P[b] + S[b]
+        for g in range(2):
+            # read back through the table: logical order must be the generator's logical sequence
+            assert np.array_equal(gather_logical(kp, w.compact_table[b], L, g),
+                                  storage_to_f64(w.logical_k[b][:, g]))
+            assert np.array_equal(gather_logical(vp, w.compact_table[b], L, g),
+                                  storage_to_f64(w.logical_v[b][:, g]))
+        for j in range(P[b], L):
+            touched[w.compact_table[b, j // 16], :, j % 16] = True
+    # every other byte unchanged (including the NaN canaries and prefix slots)
+    assert np.array_equal(kp[~touched], w.k_pool_c[~touched])
+    assert np.array_equal(vp[~touched], w.v_pool_c[~touched])
+    # the slots that were written held NaN before (fresh slots only)
+    assert np.all(w.k_pool_c[touched] == 0x7FC0)
+
+
+def test_append_leaves_shared_fork_blocks_alone():
+    """Forked sequences share their first pages (§5.2); appending into every
+    child must not change a byte of the shared pages."""
+    w = build_workload(name="fork", seed=22, prefix_len=[48, 60, 33], suffix_len=[9, 20, 40], num_q_heads=2,
+                       num_kv_heads=1, head_dim=8, dtype="bf16", num_blocks=64, shared_prefix_blocks=2)
+    kp, vp = _appended(w)
+    shared = w.compact_table[0, :2]
+    assert np.all(w.compact_table[:, :2] == shared)
+    assert np.array_equal(kp[shared], w.k_pool_c[shared]) and np.array_equal(vp[shared], w.v_pool_c[shared])
