@@ -1,0 +1,140 @@
+/*
+ * kvt.h -- paged-KV extend attention for AMD MI355X (gfx950).
+ *
+ * The computation a prefix hit leaves to do in a ReAct turn: KV reuse exists
+ * so that a long reusable prefix is not prefilled again (paper §1, §2.2); the
+ * S new tokens of the turn attend causally over the P reused positions plus
+ * themselves, and their K/V are written into freshly allocated cache pages
+ * once the tokens have taken part in inference (§5.1, §6.2).  A forked
+ * context shares its parent's pages (§5.2, §6.1); a replaced middle message
+ * invalidates the cached suffix, which is recomputed as a longer suffix over
+ * a shorter reused prefix (§5.1).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Pool: K and V of ONE layer, each [num_blocks][num_kv_heads][16][head_dim],
+ *   contiguous, head_dim fastest.  Page (block) size is 16 tokens.
+ * Sequences: B >= 1.  Sequence b reuses P_b >= 0 positions already in the
+ *   pool and adds S_b >= 1 new tokens at logical positions P_b .. P_b+S_b-1.
+ *   Logical position p of sequence b lives at slot p % 16 of physical block
+ *   block_table[b * max_blocks + p / 16].  Table entries past the last used
+ *   block are ignored (they may hold -1).
+ * Packed token rows: every per-token tensor (q, out, lse, k_new, v_new)
+ *   stores sequence b's new tokens at rows off_b .. off_b+S_b-1 with
+ *   off_b = S_0 + ... + S_{b-1}; T = sum_b S_b.
+ * GQA: query head h reads kv-head h / (Hq / Hkv) (consecutive head groups).
+ * Dtypes: q, out, k_new, v_new and both pools share the pool dtype.  bf16
+ *   inputs feed bf16 MFMA directly; fp32 inputs are rounded to bf16 (RNE) in
+ *   registers and take the same path.  Softmax and accumulation are fp32.
+ * Ownership: every buffer belongs to the caller.  The library allocates no
+ *   device memory and keeps no state between calls except a cached device
+ *   property; calls are reentrant.
+ * Asynchrony: KVT_OK means the work is enqueued on `stream` (a hipStream_t;
+ *   NULL = the default stream).  Device-side faults surface at the caller's
+ *   next synchronisation.  Pool pages read or written by a call must not be
+ *   freed or reused until the stream has passed the call.
+ * Errors: every argument check runs on the host before any HIP call; on a
+ *   non-OK return nothing has been enqueued.  KVT_ERR_DEVICE reports a failed
+ *   launch; kvt_last_hip_error() then returns the hipError_t (per thread).
+ * Unchecked block ids: without a host mirror of the block table (checked
+ *   mode off), an out-of-range id is never dereferenced: extend reads zeros
+ *   for it and append skips it; the result is then unspecified, not a fault.
+ */
+#ifndef KVT_H_
+#define KVT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KVT_BLOCK_SIZE 16
+
+typedef enum {
+  KVT_OK = 0,
+  KVT_ERR_INVALID_ARG = 1,   /* null pointer, bad length, table too narrow, aliasing */
+  KVT_ERR_UNSUPPORTED = 2,   /* head_dim not in {64,128}, unknown dtype */
+  KVT_ERR_OUT_OF_RANGE = 3,  /* checked mode: block id outside [0,num_blocks) or duplicate append slot */
+  KVT_ERR_WORKSPACE = 4,     /* non-null workspace smaller than kvt_extend_workspace_bytes() */
+  KVT_ERR_DEVICE = 5         /* HIP launch failure; see kvt_last_hip_error() */
+} kvt_status;
+
+typedef enum { KVT_DTYPE_BF16 = 0, KVT_DTYPE_F32 = 1 } kvt_dtype;
+
+/* The paged KV pool of one layer. */
+typedef struct {
+  void*   k;             /* device, [num_blocks][num_kv_heads][16][head_dim] */
+  void*   v;             /* device, same shape and dtype as k */
+  int64_t num_blocks;    /* >= 1; 64-bit: 2^20 bf16 blocks span 32 GiB */
+  int32_t num_kv_heads;  /* Hkv >= 1 */
+  int32_t head_dim;      /* D in {64, 128} */
+  int32_t dtype;         /* kvt_dtype of k, v and every per-token tensor */
+} kvt_pool;
+
+/* The sequences of one call. */
+typedef struct {
+  int32_t        num_seqs;          /* B >= 1 */
+  const int32_t* prefix_len;        /* HOST [B], P_b >= 0: positions already in the pool */
+  const int32_t* suffix_len;        /* HOST [B], S_b >= 1: new tokens of this call */
+  const int32_t* block_table;       /* DEVICE [B][max_blocks], row-major physical block ids */
+  const int32_t* block_table_host;  /* HOST copy of block_table, or NULL; non-NULL turns on checked mode */
+  int32_t        max_blocks;        /* row stride; ceil((P_b+S_b)/16) <= max_blocks for every b */
+} kvt_seqs;
+
+/*
+ * kvt_append_kv -- write the new tokens' K/V into their pages.
+ *
+ * For every b, t < S_b, kv-head g, with p = P_b + t:
+ *   k_pool[block_table[b][p/16]][g][p%16][:] = k_new[off_b + t][g][:]  (same for v)
+ * a bitwise copy.  k_new, v_new: device [T][Hkv][D] in the pool dtype.
+ * No other pool byte is written.  Targets must be distinct across the call
+ * (checked mode rejects a repeated (block, slot) with KVT_ERR_OUT_OF_RANGE);
+ * blocks shared by several sequences (a fork) are read-only here as long as
+ * no sequence's new positions fall in them.
+ */
+kvt_status kvt_append_kv(const kvt_pool* pool, const kvt_seqs* seqs,
+                         const void* k_new, const void* v_new, void* stream);
+
+/*
+ * kvt_extend_attention -- causal attention of the new tokens over prefix + suffix.
+ *
+ * For every b, new token i < S_b, query head h (g = h / (Hq/Hkv)):
+ *   s_j = scale * <q[off_b+i][h], K_b[j]>,  j = 0 .. P_b + i  (own position included)
+ *   out[off_b+i][h] = sum_j softmax(s)_j V_b[j]
+ *   lse[off_b+i][h] = ln sum_j exp(s_j)            (natural log; optional)
+ * K_b/V_b are read through the block table; both the reused prefix and this
+ * call's suffix come from the pool, so kvt_append_kv for the same tokens must
+ * be enqueued first (same stream, or otherwise ordered before this call).
+ *
+ * q: device [T][Hq][D]; out: device [T][Hq][D] (may not overlap q or a pool);
+ * lse: device float [T][Hq] or NULL.  num_q_heads must be a multiple of Hkv.
+ * scale: finite and > 0 (usually 1/sqrt(D)).
+ * workspace: device scratch for split-key partial results.  Pass NULL/0 to
+ * run without splitting; otherwise workspace_bytes must be at least
+ * kvt_extend_workspace_bytes() for the same arguments (else
+ * KVT_ERR_WORKSPACE).  The split decision depends only on the lengths and
+ * shapes, so results are bit-reproducible for given arguments.
+ */
+kvt_status kvt_extend_attention(const kvt_pool* pool, const kvt_seqs* seqs,
+                                const void* q, int32_t num_q_heads, float scale,
+                                void* out, float* lse,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace that lets kvt_extend_attention split long key ranges over more
+ * workgroups (short suffixes, small batches).  0 when no split is planned or
+ * the arguments are invalid.  Host-only; enqueues nothing. */
+size_t kvt_extend_workspace_bytes(const kvt_pool* pool, const kvt_seqs* seqs, int32_t num_q_heads);
+
+/* Static English text for a status code (never NULL). */
+const char* kvt_status_str(kvt_status s);
+
+/* hipError_t of the last KVT_ERR_DEVICE returned on this thread (0 if none). */
+int kvt_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVT_H_ */

@@ -1,0 +1,308 @@
+// C-ABI entry points: argument validation, work planning and launches.
+//
+// Every check runs on the host before the first HIP call, so a bad call
+// returns an error with nothing enqueued.  Planning is host arithmetic only:
+// sequences are ordered longest first, the (row tile, key split) units of
+// each sequence are numbered longest first, and the kv-head index varies
+// fastest over workgroup ids -- workgroups are dispatched round-robin over the
+// 8 XCDs, so with 8 (or a multiple/divisor of 8) kv-heads every workgroup of
+// one kv-head runs on the same XCD and its K/V stream is shared in that L2.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <numeric>
+#include <unordered_set>
+#include <vector>
+
+#include "kvt.h"
+#include "kvt_internal.h"
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+kvt_status device_error(hipError_t e) {
+  g_last_hip_error = (int)e;
+  return KVT_ERR_DEVICE;
+}
+
+int elem_bytes(int32_t dtype) { return dtype == KVT_DTYPE_BF16 ? 2 : 4; }
+
+// Number of compute units of the current device, queried once per device.
+int device_cus() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) { (void)hipGetLastError(); return 256; }
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) {
+      (void)hipGetLastError();
+      n = 256;
+    }
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
+kvt_status check_pool(const kvt_pool* pool) {
+  if (pool == nullptr || pool->k == nullptr || pool->v == nullptr) return KVT_ERR_INVALID_ARG;
+  if (pool->num_blocks < 1 || pool->num_kv_heads < 1) return KVT_ERR_INVALID_ARG;
+  if (pool->head_dim != 64 && pool->head_dim != 128) return KVT_ERR_UNSUPPORTED;
+  if (pool->dtype != KVT_DTYPE_BF16 && pool->dtype != KVT_DTYPE_F32) return KVT_ERR_UNSUPPORTED;
+  return KVT_OK;
+}
+
+// Validates lengths and table width; fills the total token count.
+kvt_status check_seqs(const kvt_seqs* seqs, int64_t* total_tokens) {
+  if (seqs == nullptr || seqs->num_seqs < 1) return KVT_ERR_INVALID_ARG;
+  if (seqs->prefix_len == nullptr || seqs->suffix_len == nullptr || seqs->block_table == nullptr)
+    return KVT_ERR_INVALID_ARG;
+  if (seqs->max_blocks < 1) return KVT_ERR_INVALID_ARG;
+  int64_t T = 0;
+  for (int b = 0; b < seqs->num_seqs; ++b) {
+    const int64_t P = seqs->prefix_len[b], S = seqs->suffix_len[b];
+    if (P < 0 || S < 1) return KVT_ERR_INVALID_ARG;
+    const int64_t L = P + S;
+    if (L > INT32_MAX / 2) return KVT_ERR_INVALID_ARG;
+    if ((L + kvt::kBlock - 1) / kvt::kBlock > seqs->max_blocks) return KVT_ERR_INVALID_ARG;
+    T += S;
+  }
+  if (T > INT32_MAX / 2) return KVT_ERR_INVALID_ARG;
+  *total_tokens = T;
+  return KVT_OK;
+}
+
+// Checked mode: every used block id is inside the pool.
+kvt_status check_table_ids(const kvt_pool* pool, const kvt_seqs* seqs) {
+  if (seqs->block_table_host == nullptr) return KVT_OK;
+  for (int b = 0; b < seqs->num_seqs; ++b) {
+    const int64_t L = (int64_t)seqs->prefix_len[b] + seqs->suffix_len[b];
+    const int64_t nblk = (L + kvt::kBlock - 1) / kvt::kBlock;
+    const int32_t* row = seqs->block_table_host + (int64_t)b * seqs->max_blocks;
+    for (int64_t i = 0; i < nblk; ++i)
+      if (row[i] < 0 || (int64_t)row[i] >= pool->num_blocks) return KVT_ERR_OUT_OF_RANGE;
+  }
+  return KVT_OK;
+}
+
+bool overlaps(const void* a, size_t an, const void* b, size_t bn) {
+  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x < y + bn && y < x + an;
+}
+
+struct ExtendPlan {
+  int nsplit = 1;
+  std::vector<int> order;   // sequences, longest key range first
+  size_t ws_bytes = 0;      // workspace needed for nsplit > 1
+};
+
+int row_tiles(int32_t suffix, int group) {
+  const int64_t rows = (int64_t)suffix * group;
+  return (int)((rows + kvt::kExtTileRows - 1) / kvt::kExtTileRows);
+}
+
+// Split long key ranges only when the row tiles alone cannot fill the chip.
+ExtendPlan make_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t num_q_heads, int64_t T) {
+  ExtendPlan p;
+  const int B = seqs->num_seqs;
+  const int G = num_q_heads / pool->num_kv_heads;
+  p.order.resize(B);
+  std::iota(p.order.begin(), p.order.end(), 0);
+  std::stable_sort(p.order.begin(), p.order.end(), [&](int x, int y) {
+    return (int64_t)seqs->prefix_len[x] + seqs->suffix_len[x] > (int64_t)seqs->prefix_len[y] + seqs->suffix_len[y];
+  });
+  int64_t units = 0;
+  int64_t min_keys = INT64_MAX;
+  for (int b = 0; b < B; ++b) {
+    units += (int64_t)row_tiles(seqs->suffix_len[b], G) * pool->num_kv_heads;
+    min_keys = std::min<int64_t>(min_keys, (int64_t)seqs->prefix_len[b] + 1);
+  }
+  const int cus = device_cus();
+  int ns = 1;
+  if (units < cus) {
+    ns = (int)((cus + units - 1) / units);
+    // each split keeps at least 16 key tiles (1024 keys) of the shortest sequence
+    const int64_t by_keys = std::max<int64_t>(1, min_keys / (16 * kvt::kExtKeysPerTile));
+    ns = (int)std::min<int64_t>({(int64_t)ns, by_keys, (int64_t)kvt::kMaxSplits});
+    ns = std::max(ns, 1);
+  }
+  p.nsplit = ns;
+  if (ns > 1) {
+    const int64_t rows = T * num_q_heads;
+    const size_t o_bytes = (size_t)ns * rows * pool->head_dim * sizeof(float);
+    const size_t ml_bytes = (size_t)ns * rows * 2 * sizeof(float);
+    p.ws_bytes = ((o_bytes + 255) / 256) * 256 + ml_bytes;
+  }
+  return p;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* kvt_status_str(kvt_status s) {
+  switch (s) {
+    case KVT_OK: return "ok";
+    case KVT_ERR_INVALID_ARG: return "invalid argument";
+    case KVT_ERR_UNSUPPORTED: return "unsupported shape or dtype";
+    case KVT_ERR_OUT_OF_RANGE: return "block id out of range or duplicate append target";
+    case KVT_ERR_WORKSPACE: return "workspace too small";
+    case KVT_ERR_DEVICE: return "HIP launch failed";
+  }
+  return "unknown status";
+}
+
+int kvt_last_hip_error(void) { return g_last_hip_error; }
+
+kvt_status kvt_append_kv(const kvt_pool* pool, const kvt_seqs* seqs, const void* k_new, const void* v_new,
+                         void* stream) {
+  kvt_status st = check_pool(pool);
+  if (st != KVT_OK) return st;
+  int64_t T = 0;
+  if ((st = check_seqs(seqs, &T)) != KVT_OK) return st;
+  if (k_new == nullptr || v_new == nullptr) return KVT_ERR_INVALID_ARG;
+  if ((st = check_table_ids(pool, seqs)) != KVT_OK) return st;
+  const size_t pool_bytes = (size_t)pool->num_blocks * pool->num_kv_heads * kvt::kBlock * pool->head_dim *
+                            elem_bytes(pool->dtype);
+  const size_t new_bytes = (size_t)T * pool->num_kv_heads * pool->head_dim * elem_bytes(pool->dtype);
+  for (const void* src : {k_new, v_new})
+    for (const void* dst : {(const void*)pool->k, (const void*)pool->v})
+      if (overlaps(src, new_bytes, dst, pool_bytes)) return KVT_ERR_INVALID_ARG;
+  if (seqs->block_table_host != nullptr) {
+    // two new tokens may not target one (block, slot)
+    std::unordered_set<int64_t> seen;
+    seen.reserve((size_t)T * 2);
+    for (int b = 0; b < seqs->num_seqs; ++b) {
+      const int32_t* row = seqs->block_table_host + (int64_t)b * seqs->max_blocks;
+      for (int32_t t = 0; t < seqs->suffix_len[b]; ++t) {
+        const int64_t pos = (int64_t)seqs->prefix_len[b] + t;
+        const int64_t key = (int64_t)row[pos / kvt::kBlock] * kvt::kBlock + pos % kvt::kBlock;
+        if (!seen.insert(key).second) return KVT_ERR_OUT_OF_RANGE;
+      }
+    }
+  }
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  kvt::AppendArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.k_pool = pool->k;
+  a.v_pool = pool->v;
+  a.block_table = seqs->block_table;
+  a.num_blocks = pool->num_blocks;
+  a.max_blocks = seqs->max_blocks;
+  a.num_kv_heads = pool->num_kv_heads;
+  int32_t row = 0;
+  for (int b0 = 0; b0 < seqs->num_seqs; b0 += kvt::kSeqsPerLaunch) {
+    const int n = std::min(kvt::kSeqsPerLaunch, seqs->num_seqs - b0);
+    a.nseq = n;
+    a.row_begin = row;
+    for (int i = 0; i < n; ++i) {
+      const int b = b0 + i;
+      a.seq[i] = kvt::SeqDesc{b, seqs->prefix_len[b], seqs->suffix_len[b], row};
+      row += seqs->suffix_len[b];
+    }
+    a.rows = row - a.row_begin;
+    const hipError_t e = kvt::launch_append(a, pool->dtype, pool->head_dim, s);
+    if (e != hipSuccess) return device_error(e);
+  }
+  return KVT_OK;
+}
+
+size_t kvt_extend_workspace_bytes(const kvt_pool* pool, const kvt_seqs* seqs, int32_t num_q_heads) {
+  if (check_pool(pool) != KVT_OK) return 0;
+  int64_t T = 0;
+  if (check_seqs(seqs, &T) != KVT_OK) return 0;
+  if (num_q_heads < 1 || num_q_heads % pool->num_kv_heads != 0) return 0;
+  return make_plan(pool, seqs, num_q_heads, T).ws_bytes;
+}
+
+kvt_status kvt_extend_attention(const kvt_pool* pool, const kvt_seqs* seqs, const void* q, int32_t num_q_heads,
+                                float scale, void* out, float* lse, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  kvt_status st = check_pool(pool);
+  if (st != KVT_OK) return st;
+  int64_t T = 0;
+  if ((st = check_seqs(seqs, &T)) != KVT_OK) return st;
+  if (q == nullptr || out == nullptr) return KVT_ERR_INVALID_ARG;
+  if (num_q_heads < 1 || num_q_heads % pool->num_kv_heads != 0) return KVT_ERR_INVALID_ARG;
+  if (!(scale > 0.f) || !std::isfinite(scale)) return KVT_ERR_INVALID_ARG;
+  if ((st = check_table_ids(pool, seqs)) != KVT_OK) return st;
+  const size_t es = elem_bytes(pool->dtype);
+  const size_t tok_bytes = (size_t)T * num_q_heads * pool->head_dim * es;
+  const size_t pool_bytes = (size_t)pool->num_blocks * pool->num_kv_heads * kvt::kBlock * pool->head_dim * es;
+  if (overlaps(out, tok_bytes, q, tok_bytes) || overlaps(out, tok_bytes, pool->k, pool_bytes) ||
+      overlaps(out, tok_bytes, pool->v, pool_bytes))
+    return KVT_ERR_INVALID_ARG;
+  if (lse != nullptr && overlaps(lse, (size_t)T * num_q_heads * sizeof(float), out, tok_bytes))
+    return KVT_ERR_INVALID_ARG;
+
+  ExtendPlan plan = make_plan(pool, seqs, num_q_heads, T);
+  if (plan.nsplit > 1) {
+    if (workspace == nullptr && workspace_bytes == 0) {
+      plan.nsplit = 1;   // no scratch offered: run unsplit
+    } else if (workspace == nullptr || workspace_bytes < plan.ws_bytes) {
+      return KVT_ERR_WORKSPACE;
+    }
+  }
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const int G = num_q_heads / pool->num_kv_heads;
+  std::vector<int32_t> row_off(seqs->num_seqs + 1, 0);
+  for (int b = 0; b < seqs->num_seqs; ++b) row_off[b + 1] = row_off[b] + seqs->suffix_len[b];
+
+  kvt::ExtendArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.q = q;
+  a.k_pool = pool->k;
+  a.v_pool = pool->v;
+  a.out = out;
+  a.lse = lse;
+  a.block_table = seqs->block_table;
+  a.num_blocks = pool->num_blocks;
+  a.max_blocks = seqs->max_blocks;
+  a.num_q_heads = num_q_heads;
+  a.num_kv_heads = pool->num_kv_heads;
+  a.group = G;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.nsplit = plan.nsplit;
+  a.total_rows = (int32_t)T;
+  if (plan.nsplit > 1) {
+    const size_t o_bytes = (size_t)plan.nsplit * T * num_q_heads * pool->head_dim * sizeof(float);
+    a.part_o = reinterpret_cast<float*>(workspace);
+    a.part_ml = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + ((o_bytes + 255) / 256) * 256);
+  }
+  for (size_t c0 = 0; c0 < plan.order.size(); c0 += kvt::kSeqsPerLaunch) {
+    const int n = (int)std::min<size_t>(kvt::kSeqsPerLaunch, plan.order.size() - c0);
+    a.nseq = n;
+    int32_t units = 0;
+    for (int i = 0; i < n; ++i) {
+      const int b = plan.order[c0 + i];
+      a.seq[i] = kvt::SeqDesc{b, seqs->prefix_len[b], seqs->suffix_len[b], row_off[b]};
+      a.unit_begin[i] = units;
+      units += row_tiles(seqs->suffix_len[b], G) * plan.nsplit;
+    }
+    a.unit_begin[n] = units;
+    const int64_t grid = (int64_t)units * pool->num_kv_heads;
+    if (grid > INT32_MAX) return KVT_ERR_INVALID_ARG;
+    const hipError_t e = kvt::launch_extend(a, pool->dtype, pool->head_dim, (int)grid, s);
+    if (e != hipSuccess) return device_error(e);
+  }
+  if (plan.nsplit > 1) {
+    kvt::CombineArgs c;
+    c.part_o = a.part_o;
+    c.part_ml = a.part_ml;
+    c.out = out;
+    c.lse = lse;
+    c.rows = T * num_q_heads;
+    c.nsplit = plan.nsplit;
+    const hipError_t e = kvt::launch_combine(c, pool->dtype, pool->head_dim, s);
+    if (e != hipSuccess) return device_error(e);
+  }
+  return KVT_OK;
+}
+
+}  // extern "C"

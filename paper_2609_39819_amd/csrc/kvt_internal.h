@@ -1,0 +1,81 @@
+// Launch descriptors shared by the host dispatcher (kvt_api.cpp) and the
+// device code (kvt_append.hip, kvt_extend.hip).  Per-call sequence metadata
+// travels by value in the kernel arguments, so a call needs no device
+// allocation and no host-to-device copy; calls with more sequences than one
+// descriptor holds are split over several launches.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kvt {
+
+constexpr int kBlock = 16;          // tokens per cache page
+constexpr int kSeqsPerLaunch = 64;  // sequences described by one launch
+
+// Extend tiling: one workgroup = 8 waves x 32 packed query rows, 64-key tiles.
+constexpr int kExtWaves = 8;
+constexpr int kExtRowsPerWave = 32;
+constexpr int kExtTileRows = kExtWaves * kExtRowsPerWave;   // 256
+constexpr int kExtKeysPerTile = 64;
+constexpr int kMaxSplits = 16;
+
+struct SeqDesc {
+  int32_t seq;      // row of the block table
+  int32_t prefix;   // P_b
+  int32_t suffix;   // S_b
+  int32_t row_off;  // first packed token row of the sequence (whole call)
+};
+
+struct AppendArgs {
+  const void* k_new;
+  const void* v_new;
+  void* k_pool;
+  void* v_pool;
+  const int32_t* block_table;
+  int64_t num_blocks;
+  int32_t max_blocks;
+  int32_t num_kv_heads;
+  int32_t row_begin;  // first packed row covered by this launch
+  int32_t rows;       // rows covered by this launch
+  int32_t nseq;
+  SeqDesc seq[kSeqsPerLaunch];  // in packed-row order
+};
+
+struct ExtendArgs {
+  const void* q;
+  const void* k_pool;
+  const void* v_pool;
+  void* out;
+  float* lse;        // may be null
+  float* part_o;     // [nsplit][total_rows * Hq][D] when nsplit > 1
+  float* part_ml;    // [nsplit][total_rows * Hq][2]  (running max in log2 units, row sum)
+  const int32_t* block_table;
+  int64_t num_blocks;
+  int32_t max_blocks;
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t group;        // Hq / Hkv
+  float scale_log2;     // scale * log2(e)
+  int32_t nsplit;
+  int32_t total_rows;   // T of the whole call
+  int32_t nseq;
+  int32_t unit_begin[kSeqsPerLaunch + 1];  // prefix sums of (row tiles x nsplit), longest first
+  SeqDesc seq[kSeqsPerLaunch];
+};
+
+struct CombineArgs {
+  const float* part_o;
+  const float* part_ml;
+  void* out;
+  float* lse;
+  int64_t rows;    // T * Hq
+  int32_t nsplit;
+};
+
+// Launchers (device code files).  Return the launch status.
+hipError_t launch_append(const AppendArgs& a, int dtype, int head_dim, hipStream_t stream);
+hipError_t launch_extend(const ExtendArgs& a, int dtype, int head_dim, int grid, hipStream_t stream);
+hipError_t launch_combine(const CombineArgs& a, int dtype, int head_dim, hipStream_t stream);
+
+}  // namespace kvt

@@ -1,0 +1,210 @@
+"""Python binding of ``libkvt.so`` (argument marshalling only).
+
+Every step of append and extend attention runs in the library's HIP
+kernels; this module turns torch tensors into the C structs of
+``include/kvt.h``, passes torch's current HIP stream, and raises on a
+non-OK status.  torch supplies device memory and streams, nothing else.
+There is no fallback: if the library is missing, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkvt.so")
+
+KVT_OK = 0
+KVT_ERR_INVALID_ARG = 1
+KVT_ERR_UNSUPPORTED = 2
+KVT_ERR_OUT_OF_RANGE = 3
+KVT_ERR_WORKSPACE = 4
+KVT_ERR_DEVICE = 5
+KVT_DTYPE_BF16 = 0
+KVT_DTYPE_F32 = 1
+BLOCK_SIZE = 16
+
+EXPORTED = ("kvt_append_kv", "kvt_extend_attention", "kvt_extend_workspace_bytes",
+            "kvt_status_str", "kvt_last_hip_error")
+
+
+class KvtPool(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("num_blocks", ctypes.c_int64),
+                ("num_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class KvtSeqs(ctypes.Structure):
+    _fields_ = [("num_seqs", ctypes.c_int32), ("prefix_len", ctypes.POINTER(ctypes.c_int32)),
+                ("suffix_len", ctypes.POINTER(ctypes.c_int32)), ("block_table", ctypes.c_void_p),
+                ("block_table_host", ctypes.POINTER(ctypes.c_int32)), ("max_blocks", ctypes.c_int32)]
+
+
+class KvtError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {status_str(status)} (status {status}"
+                         + (f", hipError {lib().kvt_last_hip_error()}" if status == KVT_ERR_DEVICE else "") + ")")
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_39819_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.POINTER
+        L.kvt_append_kv.argtypes = [P(KvtPool), P(KvtSeqs), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+        L.kvt_append_kv.restype = ctypes.c_int
+        L.kvt_extend_attention.argtypes = [P(KvtPool), P(KvtSeqs), ctypes.c_void_p, ctypes.c_int32, ctypes.c_float,
+                                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                           ctypes.c_void_p]
+        L.kvt_extend_attention.restype = ctypes.c_int
+        L.kvt_extend_workspace_bytes.argtypes = [P(KvtPool), P(KvtSeqs), ctypes.c_int32]
+        L.kvt_extend_workspace_bytes.restype = ctypes.c_size_t
+        L.kvt_status_str.argtypes = [ctypes.c_int]
+        L.kvt_status_str.restype = ctypes.c_char_p
+        L.kvt_last_hip_error.argtypes = []
+        L.kvt_last_hip_error.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_str(s: int) -> str:
+    return lib().kvt_status_str(int(s)).decode()
+
+
+# ---------------------------------------------------------------------------
+# raw structs (plain integers as pointers)
+# ---------------------------------------------------------------------------
+
+def _i32_array(x) -> ctypes.Array:
+    a = np.ascontiguousarray(np.asarray(x, dtype=np.int32).reshape(-1))
+    return (ctypes.c_int32 * a.size)(*a.tolist())
+
+
+def raw_pool(k: int, v: int, num_blocks: int, num_kv_heads: int, head_dim: int, dtype: int) -> KvtPool:
+    return KvtPool(k, v, num_blocks, num_kv_heads, head_dim, dtype)
+
+
+class RawSeqs:
+    """kvt_seqs plus the host arrays it points at (kept alive with it)."""
+
+    def __init__(self, prefix_len, suffix_len, block_table_ptr: int, max_blocks: int, block_table_host=None):
+        self.prefix = _i32_array(prefix_len)
+        self.suffix = _i32_array(suffix_len)
+        self.host = _i32_array(block_table_host) if block_table_host is not None else None
+        self.struct = KvtSeqs(len(self.prefix), self.prefix, self.suffix, block_table_ptr,
+                              self.host if self.host is not None else None, max_blocks)
+
+
+# ---------------------------------------------------------------------------
+# torch-facing calls
+# ---------------------------------------------------------------------------
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return KVT_DTYPE_BF16
+    if t.dtype == torch.float32:
+        return KVT_DTYPE_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _stream_handle(device, stream=None) -> int:
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    return s.cuda_stream
+
+
+def _pool_struct(k_pool, v_pool) -> KvtPool:
+    if k_pool.shape != v_pool.shape or k_pool.dtype != v_pool.dtype or k_pool.dim() != 4:
+        raise ValueError("k_pool and v_pool must both be [num_blocks][num_kv_heads][16][head_dim] of one dtype")
+    if k_pool.shape[2] != BLOCK_SIZE:
+        raise ValueError("page size must be 16")
+    if not (k_pool.is_contiguous() and v_pool.is_contiguous()):
+        raise ValueError("pools must be contiguous")
+    nb, hkv, _, d = k_pool.shape
+    return KvtPool(k_pool.data_ptr(), v_pool.data_ptr(), nb, hkv, d, _dtype_code(k_pool))
+
+
+def _seqs(prefix_len, suffix_len, block_table, checked: bool) -> RawSeqs:
+    import torch
+    if block_table.dtype != torch.int32 or block_table.dim() != 2 or not block_table.is_contiguous():
+        raise ValueError("block_table must be a contiguous int32 [num_seqs][max_blocks] device tensor")
+    host = block_table.cpu().numpy() if checked else None
+    return RawSeqs(prefix_len, suffix_len, block_table.data_ptr(), block_table.shape[1], host)
+
+
+def _check_tokens(t, name, rows, heads, d, dtype):
+    if t.dtype != dtype or tuple(t.shape) != (rows, heads, d) or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous [{rows}][{heads}][{d}] {dtype} tensor, got {tuple(t.shape)} {t.dtype}")
+
+
+def append_kv(k_pool, v_pool, block_table, prefix_len: Sequence[int], suffix_len: Sequence[int], k_new, v_new,
+              *, stream=None, checked: bool = False) -> None:
+    """Scatter the new tokens' K/V into their pages (``kvt_append_kv``)."""
+    pool = _pool_struct(k_pool, v_pool)
+    seqs = _seqs(prefix_len, suffix_len, block_table, checked)
+    T = int(np.sum(np.asarray(suffix_len, dtype=np.int64)))
+    _check_tokens(k_new, "k_new", T, pool.num_kv_heads, pool.head_dim, k_pool.dtype)
+    _check_tokens(v_new, "v_new", T, pool.num_kv_heads, pool.head_dim, k_pool.dtype)
+    st = lib().kvt_append_kv(ctypes.byref(pool), ctypes.byref(seqs.struct), k_new.data_ptr(), v_new.data_ptr(),
+                             _stream_handle(k_pool.device, stream))
+    if st != KVT_OK:
+        raise KvtError(st, "kvt_append_kv")
+
+
+def extend_workspace_bytes(k_pool, v_pool, block_table, prefix_len, suffix_len, num_q_heads: int) -> int:
+    pool = _pool_struct(k_pool, v_pool)
+    seqs = _seqs(prefix_len, suffix_len, block_table, False)
+    return int(lib().kvt_extend_workspace_bytes(ctypes.byref(pool), ctypes.byref(seqs.struct), int(num_q_heads)))
+
+
+def extend_attention(q, k_pool, v_pool, block_table, prefix_len: Sequence[int], suffix_len: Sequence[int],
+                     scale: Optional[float] = None, *, out=None, lse=None, return_lse: bool = False,
+                     workspace=None, use_workspace: bool = True, stream=None, checked: bool = False):
+    """Causal attention of the new tokens over prefix + suffix (``kvt_extend_attention``).
+
+    Returns ``out`` ([T][Hq][D], pool dtype), or ``(out, lse)`` when an lse
+    buffer is given or ``return_lse`` is set.  ``workspace``: a byte tensor
+    of at least ``extend_workspace_bytes`` (allocated here when
+    ``use_workspace`` and none is given).
+    """
+    import torch
+    pool = _pool_struct(k_pool, v_pool)
+    seqs = _seqs(prefix_len, suffix_len, block_table, checked)
+    T = int(np.sum(np.asarray(suffix_len, dtype=np.int64)))
+    Hq = int(q.shape[1])
+    _check_tokens(q, "q", T, Hq, pool.head_dim, k_pool.dtype)
+    if scale is None:
+        scale = 1.0 / math.sqrt(pool.head_dim)
+    if out is None:
+        out = torch.empty_like(q)
+    else:
+        _check_tokens(out, "out", T, Hq, pool.head_dim, k_pool.dtype)
+    want_lse = return_lse or lse is not None
+    if want_lse and lse is None:
+        lse = torch.empty((T, Hq), dtype=torch.float32, device=q.device)
+    if lse is not None and (lse.dtype != torch.float32 or tuple(lse.shape) != (T, Hq) or not lse.is_contiguous()):
+        raise ValueError("lse must be a contiguous float32 [T][Hq] tensor")
+    ws_ptr, ws_bytes = None, 0
+    if workspace is not None:
+        ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
+    elif use_workspace:
+        need = int(lib().kvt_extend_workspace_bytes(ctypes.byref(pool), ctypes.byref(seqs.struct), Hq))
+        if need:
+            workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+            ws_ptr, ws_bytes = workspace.data_ptr(), need
+    st = lib().kvt_extend_attention(ctypes.byref(pool), ctypes.byref(seqs.struct), q.data_ptr(), Hq, float(scale),
+                                    out.data_ptr(), lse.data_ptr() if lse is not None else None, ws_ptr, ws_bytes,
+                                    _stream_handle(q.device, stream))
+    if st != KVT_OK:
+        raise KvtError(st, "kvt_extend_attention")
+    return (out, lse) if want_lse else out

@@ -1,0 +1,179 @@
+"""C-ABI library: it loads, exports every declared symbol, and rejects bad
+arguments on the host before any HIP call (CPU only).
+
+The pointers used here are fake; each call is built to fail validation, so no
+kernel is ever launched.  Every test that passes fake pointers is skipped
+when a GPU is present, so that a validation bug could never launch a kernel
+on them.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2609_39819_amd import kvt
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kvt.h")
+
+FAKE_K, FAKE_V, FAKE_BT = 0x10000000, 0x20000000000, 0x30000000000
+FAKE_Q, FAKE_OUT = 0x40000000000, 0x50000000000
+
+
+def _gpu_present():
+    try:
+        import torch
+        return torch.cuda.device_count() > 0
+    except Exception:
+        return False
+
+
+no_gpu_only = pytest.mark.skipif(_gpu_present(), reason="fake-pointer late-validation test runs only without a GPU")
+
+
+def declared_symbols():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(kvt_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_expected_entry_points():
+    assert declared_symbols() == sorted(kvt.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    L = kvt.lib()
+    for name in declared_symbols():
+        assert hasattr(L, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", kvt.LIB_PATH], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\bT (kvt_[a-z_]+)\b", out))
+    assert set(declared_symbols()) <= exported
+
+
+def test_status_strings():
+    for code in range(6):
+        assert kvt.status_str(code)
+    assert kvt.status_str(99) == "unknown status"
+    assert kvt.lib().kvt_last_hip_error() == 0
+
+
+def _pool(nb=64, hkv=1, d=64, dtype=kvt.KVT_DTYPE_BF16, k=FAKE_K, v=FAKE_V):
+    return kvt.raw_pool(k, v, nb, hkv, d, dtype)
+
+
+def _extend(pool, seqs, hq=4, scale=0.125, q=FAKE_Q, out=FAKE_OUT, ws=None, ws_bytes=0):
+    L = kvt.lib()
+    return L.kvt_extend_attention(ctypes.byref(pool) if pool is not None else None,
+                                  ctypes.byref(seqs.struct) if seqs is not None else None,
+                                  q, hq, scale, out, None, ws, ws_bytes, None)
+
+
+def _append(pool, seqs, kn=FAKE_Q, vn=FAKE_OUT):
+    L = kvt.lib()
+    return L.kvt_append_kv(ctypes.byref(pool) if pool is not None else None,
+                           ctypes.byref(seqs.struct) if seqs is not None else None, kn, vn, None)
+
+
+def _seqs(P=(240,), S=(16,), bt=FAKE_BT, max_blocks=16, host=None):
+    return kvt.RawSeqs(list(P), list(S), bt, max_blocks, host)
+
+
+@no_gpu_only
+@pytest.mark.parametrize("call", [_extend, _append])
+def test_invalid_arguments_are_rejected(call):
+    E = kvt.KVT_ERR_INVALID_ARG
+    assert call(None, _seqs()) == E
+    assert call(_pool(k=0), _seqs()) == E
+    assert call(_pool(nb=0), _seqs()) == E
+    assert call(_pool(hkv=0), _seqs()) == E
+    assert call(_pool(), None) == E
+    assert call(_pool(), _seqs(P=(), S=())) == E                    # no sequences
+    assert call(_pool(), _seqs(S=(0,))) == E                         # empty suffix
+    assert call(_pool(), _seqs(P=(-1,))) == E                        # negative prefix
+    assert call(_pool(), _seqs(bt=0)) == E                           # no block table
+    assert call(_pool(), _seqs(max_blocks=15)) == E                  # 256 tokens need 16 pages
+
+
+@no_gpu_only
+def test_unsupported_shapes_are_rejected():
+    U = kvt.KVT_ERR_UNSUPPORTED
+    for call in (_extend, _append):
+        assert call(_pool(d=96), _seqs()) == U
+        assert call(_pool(d=256), _seqs()) == U
+        assert call(_pool(dtype=7), _seqs()) == U
+
+
+@no_gpu_only
+def test_extend_specific_checks():
+    E = kvt.KVT_ERR_INVALID_ARG
+    assert _extend(_pool(), _seqs(), q=0) == E
+    assert _extend(_pool(), _seqs(), out=0) == E
+    assert _extend(_pool(hkv=2), _seqs(), hq=3) == E                 # Hq not a multiple of Hkv
+    assert _extend(_pool(), _seqs(), hq=0) == E
+    assert _extend(_pool(), _seqs(), scale=0.0) == E
+    assert _extend(_pool(), _seqs(), scale=-1.0) == E
+    assert _extend(_pool(), _seqs(), scale=float("nan")) == E
+    assert _extend(_pool(), _seqs(), scale=float("inf")) == E
+    assert _extend(_pool(), _seqs(), out=FAKE_Q + 64) == E           # out overlaps q
+    assert _extend(_pool(), _seqs(), out=FAKE_K + 128) == E          # out inside the K pool
+
+
+@no_gpu_only
+def test_append_specific_checks():
+    E = kvt.KVT_ERR_INVALID_ARG
+    assert _append(_pool(), _seqs(), kn=0) == E
+    assert _append(_pool(), _seqs(), vn=0) == E
+    assert _append(_pool(), _seqs(), kn=FAKE_K + 4096) == E          # source inside the pool
+
+
+@no_gpu_only
+def test_checked_mode_rejects_out_of_range_ids():
+    O = kvt.KVT_ERR_OUT_OF_RANGE
+    table = np.arange(16, dtype=np.int32).reshape(1, 16)
+    bad = table.copy(); bad[0, 7] = 64                               # pool has 64 blocks: id 64 is outside
+    assert _extend(_pool(), _seqs(host=bad)) == O
+    assert _append(_pool(), _seqs(host=bad)) == O
+    neg = table.copy(); neg[0, 0] = -1
+    assert _extend(_pool(), _seqs(host=neg)) == O
+
+
+@no_gpu_only
+def test_checked_append_rejects_two_tokens_on_one_slot():
+    # two sequences whose new positions land on the same page slot
+    host = np.array([[0, 1, 2], [5, 1, 6]], dtype=np.int32)
+    s = _seqs(P=(16, 16), S=(4, 4), max_blocks=3, host=host)
+    assert _append(_pool(), s) == kvt.KVT_ERR_OUT_OF_RANGE
+
+
+def _ws_bytes(pool, seqs, hq):
+    return kvt.lib().kvt_extend_workspace_bytes(ctypes.byref(pool), ctypes.byref(seqs.struct), hq)
+
+
+def test_workspace_bytes_follow_the_split_plan():
+    pool = _pool(nb=65536, hkv=8, d=128)
+    # short suffix (512 tokens x 32 heads): 64 row tiles -> 4 key splits
+    s = _seqs(P=(8192,), S=(512,), max_blocks=544)
+    rows = 512 * 32
+    assert _ws_bytes(pool, s, 32) == 4 * rows * 128 * 4 + 4 * rows * 2 * 4
+    # long suffix (2048 x 96 heads): 768 row tiles fill the chip, no split
+    s3 = _seqs(P=(131072,), S=(2048,), max_blocks=8320)
+    assert _ws_bytes(_pool(nb=1 << 20, hkv=8, d=128), s3, 96) == 0
+    # invalid arguments -> 0
+    assert _ws_bytes(pool, s, 33) == 0
+
+
+@no_gpu_only
+def test_small_workspace_is_rejected():
+    pool = _pool(nb=65536, hkv=8, d=128)
+    s = _seqs(P=(8192,), S=(512,), max_blocks=544)
+    assert _extend(pool, s, hq=32, scale=0.088, ws=0x60000000000, ws_bytes=16) == kvt.KVT_ERR_WORKSPACE
+
+
+def test_binding_fails_loudly_without_the_library(monkeypatch):
+    monkeypatch.setattr(kvt, "_lib", None)
+    monkeypatch.setattr(kvt, "LIB_PATH", "/nonexistent/libkvt.so")
+    with pytest.raises(RuntimeError, match="missing"):
+        kvt.lib()

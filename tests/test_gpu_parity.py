@@ -1,0 +1,194 @@
+"""GPU parity: the HIP library through the C-ABI versus the fp64 oracle.
+
+* append: bit-exact, every byte of every used page, and the NaN canaries of
+  unused pages untouched;
+* extend: max-abs <= 2e-2 and mean-abs <= 2e-3 against the oracle on the five
+  named workloads (all rows where the oracle is fast, seeded row samples at
+  full size otherwise), plus structured inputs whose closed forms expose a
+  wrong page, window or normaliser (needle, zero keys, constant values).
+"""
+import numpy as np
+import pytest
+
+from oracle import oracle_extend, storage_to_f64
+from paper_2609_39819_amd.workloads import build_workload, torch_to_np
+
+from gpu_common import (cached_config, compare, gather_rows, oracle_pools, run_append, run_extend, sample_rows,
+                        say, stage, to_f64)
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+SAMPLE = {"tiny": None, "gqa_8k": None, "react_128k": 48, "forked_agents": 6, "mutation_258k": 16}
+ALL = ["tiny", "gqa_8k", "react_128k", "forked_agents", "mutation_258k"]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    torch.cuda.set_device(0)
+    yield
+    torch.cuda.synchronize()
+
+
+def _append_check(w, d):
+    kp_o, vp_o = oracle_pools(w.name, w.variant)
+    ids = torch.from_numpy(w.phys_ids).cuda()
+    for name, dev, ref in (("k", d["k_pool"], kp_o), ("v", d["v_pool"], vp_o)):
+        got = torch_to_np(dev.index_select(0, ids), w.dtype)
+        assert np.array_equal(got.view(np.uint8), np.ascontiguousarray(ref).view(np.uint8)), f"{name} pool bytes differ"
+        # unused pages still hold the fill pattern
+        used = torch.zeros(dev.shape[0], dtype=torch.bool, device="cuda")
+        used[ids] = True
+        bits = dev.view(torch.int16 if w.dtype == "bf16" else torch.int32)
+        fill = bits[~used]
+        if fill.numel():
+            assert bool((fill == fill.reshape(-1)[0]).all()), f"{name}: an unused page was written"
+            assert bool(torch.isnan(dev[~used].reshape(-1)[:1].float()).all())
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", ALL)
+def test_append_is_bit_exact(name):
+    w = cached_config(name)
+    d = stage(w)
+    run_append(w, d)
+    _append_check(w, d)
+    del d
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", ALL)
+def test_extend_matches_oracle(name):
+    w = cached_config(name)
+    d = stage(w)
+    run_append(w, d)
+    out, lse = run_extend(w, d, return_lse=True)
+    rows = sample_rows(w, SAMPLE[name])
+    kp, vp = oracle_pools(name)
+    say(f"oracle over {sum(len(r) for r in rows)} tokens x {w.num_q_heads} heads")
+    ref_o, ref_l = oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len, w.suffix_len, w.num_kv_heads,
+                                 w.scale, rows=rows)
+    got_o = gather_rows(to_f64(out, w.dtype), w, rows)
+    got_l = gather_rows(lse.cpu().numpy().astype(np.float64), w, rows)
+    compare(got_o, ref_o, f"{name} out")
+    compare(got_l, ref_l, f"{name} lse", max_abs=2e-2, mean_abs=2e-3)
+    # every row finite, including the ones the oracle did not sample
+    assert bool(torch.isfinite(out.float()).all())
+    del d
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", ["gqa_8k", "react_128k", "forked_agents"])
+def test_needle_finds_every_page(name):
+    """q = 2 K[t]: the output is ~V[t] (O(1) values), so a wrong page, slot or
+    head mapping shows as an O(1) error instead of hiding in the 2e-2 bound."""
+    w = cached_config(name, "needle")
+    d = stage(w)
+    run_append(w, d)
+    out = run_extend(w, d)
+    rows = sample_rows(w, None if name == "gqa_8k" else 48)
+    kp, vp = oracle_pools(name, "needle")
+    ref_o, _ = oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len, w.suffix_len, w.num_kv_heads, w.scale,
+                             rows=rows)
+    got = gather_rows(to_f64(out, w.dtype), w, rows)
+    compare(got, ref_o, f"{name} needle")
+    assert np.mean(np.abs(ref_o)) > 0.5          # the needle outputs really are O(1)
+    del d
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name", ["gqa_8k", "react_128k"])
+def test_zero_keys_give_window_means(name):
+    """K = 0: out_i = mean of V over positions 0..P+i (fp64 prefix sums)."""
+    w = cached_config(name, "kzero")
+    d = stage(w)
+    run_append(w, d)
+    out = run_extend(w, d)
+    got = to_f64(out, w.dtype)
+    kp, vp = oracle_pools(name, "kzero")
+    # logical V of the single sequence, read through the compact table, prefix sums in fp64
+    P, S = int(w.prefix_len[0]), int(w.suffix_len[0])
+    G = w.group
+    ids = w.compact_table[0, :(P + S + 15) // 16]
+    for g in range(w.num_kv_heads):
+        v = storage_to_f64(vp[ids, g]).reshape(-1, w.head_dim)[:P + S]
+        cs = np.cumsum(v, axis=0)
+        n = P + np.arange(S) + 1
+        want = cs[P + np.arange(S)] / n[:, None]                 # [S, D]
+        compare(got[:, g * G:(g + 1) * G, :], np.repeat(want[:, None, :], G, axis=1), f"{name} kzero g{g}",
+                max_abs=2e-3, mean_abs=5e-4)
+    del d
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("name", ["gqa_8k", "react_128k"])
+def test_constant_values_are_reproduced(name):
+    w = cached_config(name, "vconst")
+    d = stage(w)
+    run_append(w, d)
+    out = run_extend(w, d)
+    got = to_f64(out, w.dtype)
+    c = storage_to_f64(w.extra["vconst"])
+    want = np.repeat(c, w.group, axis=0)[None]
+    # sum_j p_j c / sum_j p_j = c up to the bf16 rounding of p and of the output
+    compare(got, np.broadcast_to(want, got.shape), f"{name} vconst", max_abs=2e-2, mean_abs=2e-3)
+    assert np.max(np.abs(got - want) / np.maximum(np.abs(want), 1e-3)) < 2 ** -7
+    del d
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(600)
+def test_runs_are_bit_identical_and_split_agrees():
+    w = cached_config("gqa_8k")
+    d = stage(w)
+    run_append(w, d)
+    a = run_extend(w, d)
+    b = run_extend(w, d)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16)), "extend is not run-to-run deterministic"
+    c = run_extend(w, d, use_workspace=False)          # unsplit path
+    kp, vp = oracle_pools("gqa_8k")
+    ref, _ = oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len, w.suffix_len, w.num_kv_heads, w.scale)
+    compare(to_f64(c, w.dtype), ref, "gqa_8k unsplit")
+    compare(to_f64(a, w.dtype), to_f64(c, w.dtype), "split vs unsplit", max_abs=1e-2, mean_abs=5e-4)
+    del d
+    torch.cuda.empty_cache()
+
+
+EDGE = [
+    # (P, S, Hq, Hkv, D, dtype)
+    ([0], [1], 4, 1, 64, "bf16"),
+    ([1], [5], 4, 4, 128, "bf16"),
+    ([15], [16], 12, 1, 128, "bf16"),
+    ([16], [40], 4, 1, 64, "f32"),
+    ([17], [300], 12, 1, 128, "bf16"),
+    ([33], [1], 8, 2, 128, "f32"),
+    ([0], [700], 4, 2, 128, "bf16"),
+    ([1000, 0, 47], [70, 300, 1], 12, 1, 128, "bf16"),
+    ([63, 64, 65], [64, 65, 63], 16, 8, 64, "bf16"),
+    ([2047], [129], 2, 2, 128, "bf16"),
+]
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("case", range(len(EDGE)))
+def test_edge_shapes(case):
+    P, S, Hq, Hkv, D, dt = EDGE[case]
+    w = build_workload(name=f"edge{case}", seed=500 + case, prefix_len=P, suffix_len=S, num_q_heads=Hq,
+                       num_kv_heads=Hkv, head_dim=D, dtype=dt, num_blocks=4096)
+    d = stage(w)
+    run_append(w, d, checked=True)
+    kp, vp = w.k_pool_c, w.v_pool_c
+    from oracle import oracle_append
+    kp, vp = oracle_append(kp, vp, w.compact_table, w.prefix_len, w.suffix_len, w.k_new, w.v_new)
+    ids = torch.from_numpy(w.phys_ids).cuda()
+    assert np.array_equal(torch_to_np(d["k_pool"].index_select(0, ids), dt).view(np.uint8), kp.view(np.uint8))
+    out, lse = run_extend(w, d, return_lse=True, checked=True)
+    ref_o, ref_l = oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len, w.suffix_len, Hkv, w.scale)
+    compare(to_f64(out, dt), ref_o, f"edge{case} out")
+    compare(lse.cpu().numpy().astype(np.float64), ref_l, f"edge{case} lse")
