@@ -1,0 +1,207 @@
+"""Benchmark: one step = append the turn's new K/V + extend attention over
+the reused prefix, on one GPU, through the C-ABI library.
+
+Default workload: the long ReAct turn -- one sequence, 131072 reused prefix
+tokens, 2048 new tokens (an appended tool output), Hq=96, Hkv=8, D=128, bf16,
+pages scattered at random over a 2^20-page pool.  Prints one JSON line.
+
+  python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+``--gpus N`` with N > 1 exits: this build measures one GPU only.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "extend-attention TFLOP/s and new tokens/s at 128K reused prefix; % bf16 MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X published dense bf16 MFMA peak
+PEAK_HBM_GBPS = 8000.0
+EXTEND_SOURCES = ("paper_2609_39819_amd/csrc/kvt_extend.hip", "paper_2609_39819_amd/csrc/kvt_internal.h")
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def source_sha(paths) -> str:
+    h = hashlib.sha256()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def load_traffic(workload: str):
+    """HBM bytes per extend launch from committed rocprofv3 counters, if they
+    were taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"extend_{workload}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("source_sha256") != source_sha(EXTEND_SOURCES):
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, target_s: float):
+    """Time the fp64 oracle on a bounded sample of the same workload."""
+    from oracle import oracle_append, oracle_extend
+    from paper_2609_39819_amd.workloads import algorithmic_flops
+    try:
+        import threadpoolctl
+        threads = max([i.get("num_threads", 1) for i in threadpoolctl.threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    kp, vp = oracle_append(w.k_pool_c, w.v_pool_c, w.compact_table, w.prefix_len, w.suffix_len, w.k_new, w.v_new)
+
+    def run(n):
+        rows, flops = [], 0
+        for b in range(w.num_seqs):
+            S = int(w.suffix_len[b])
+            r = np.unique(np.linspace(0, S - 1, max(1, min(S, n))).astype(np.int64))
+            rows.append(r)
+            P = int(w.prefix_len[b])
+            flops += 4 * w.head_dim * w.num_q_heads * int((P + r + 1).sum())
+        t0 = time.perf_counter()
+        oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len, w.suffix_len, w.num_kv_heads, w.scale, rows=rows)
+        return time.perf_counter() - t0, flops, sum(len(r) for r in rows)
+
+    n = 2
+    dt, fl, nt = run(n)
+    while dt < target_s / 3 and n < int(w.suffix_len.max()):
+        n = min(int(w.suffix_len.max()), int(n * max(2.0, min(16.0, target_s / max(dt, 1e-3)))))
+        dt, fl, nt = run(n)
+    tflops = fl / dt / 1e12
+    toks = nt / dt
+    return {
+        "value": tflops, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+        "sample": f"{nt} of {w.total_tokens} new tokens (evenly spaced), all {w.num_q_heads} query heads, "
+                  f"full reused prefix; fp64 numpy oracle; {dt:.1f} s",
+        "seconds": dt, "new_tokens_per_s": toks,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="react_128k")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_39819_amd import kvt
+    from paper_2609_39819_amd.workloads import algorithmic_flops, make_config, stage_on_device
+
+    kvt.lib()   # fail loudly if the library is missing
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    log(f"generating {args.workload}")
+    t0 = time.time()
+    w = make_config(args.workload)
+    log(f"generated in {time.time() - t0:.1f}s; staging on {torch.cuda.get_device_name(dev)}")
+    d = stage_on_device(w, dev)
+    torch.cuda.synchronize()
+
+    Hq, D = w.num_q_heads, w.head_dim
+    flops = algorithmic_flops(w.prefix_len, w.suffix_len, Hq, D)
+    elem = 2 if w.dtype == "bf16" else 4
+    append_bytes = 2 * 2 * w.total_tokens * w.num_kv_heads * D * elem   # K+V, read + write
+    out = torch.empty_like(d["q"])
+    need = kvt.extend_workspace_bytes(d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.suffix_len, Hq)
+    ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev) if need else None
+    stream = torch.cuda.current_stream(dev)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        kvt.append_kv(d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.suffix_len, d["k_new"], d["v_new"])
+        if ev is not None:
+            ev[1].record(stream)
+        kvt.extend_attention(d["q"], d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.suffix_len,
+                             w.scale, out=out, workspace=ws, use_workspace=need > 0)
+        if ev is not None:
+            ev[2].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    app_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    ext_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
+    ms_per_step = wall * 1e3 / args.steps
+    value = flops / (ms_per_step * 1e-3) / 1e12
+    ext_avg = float(ext_ms.mean())
+    achieved = flops / (ext_avg * 1e-3) / 1e12
+    log(f"extend avg {ext_avg:.3f} ms (min {ext_ms.min():.3f}), append avg {app_ms.mean():.4f} ms, "
+        f"step {ms_per_step:.3f} ms, extend {achieved:.1f} TFLOP/s = {100 * achieved / PEAK_BF16_TFLOPS:.1f}% of peak")
+
+    res = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name,
+            "num_seqs": w.num_seqs,
+            "prefix_len": int(w.prefix_len.max()) if w.num_seqs == 1 else [int(x) for x in w.prefix_len],
+            "suffix_len": int(w.suffix_len.max()) if w.num_seqs == 1 else [int(x) for x in w.suffix_len],
+            "num_q_heads": Hq, "num_kv_heads": w.num_kv_heads, "head_dim": D,
+            "page_size": 16, "pool_pages": w.num_blocks, "key_splits": "auto",
+        },
+        "new_tokens_per_s": w.total_tokens / (ms_per_step * 1e-3),
+        "pct_bf16_peak": 100.0 * value / PEAK_BF16_TFLOPS,
+        "extend_ms": ext_avg,
+        "extend_tflops": achieved,
+        "append_ms": float(app_ms.mean()),
+        "append_gbps": append_bytes / (float(app_ms.mean()) * 1e-3) / 1e9,
+        "roofline": {
+            "bound": "mfma",
+            "achieved": achieved,
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS,
+            "traffic": load_traffic(w.name),
+        },
+        "gpu": torch.cuda.get_device_name(dev),
+    }
+    del d, out, ws
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        log("timing the fp64 oracle on a sample")
+        res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

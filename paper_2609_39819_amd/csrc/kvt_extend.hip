@@ -97,19 +97,34 @@ __device__ __forceinline__ float pair_sum(float x) {
   return a + b;
 }
 
+typedef __attribute__((address_space(3))) __bf16 lds_bf16;
+
+// One K/V tile of 64 keys in LDS: [K|V][key][D] bf16, 16-byte chunks of each
+// key row XOR-swizzled.  Two tiles form the double buffer; they are distinct
+// objects so the compiler can tell loads into one from reads of the other.
+template <int D>
+struct KvTile {
+  __bf16 kv[2 * kExtKeysPerTile * D];
+};
+
 template <typename T, int D>
 __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a) {
-  constexpr int KT = kExtKeysPerTile;            // 64 keys per tile
+  constexpr int KT = kExtKeysPerTile;            // 64 keys per tile = 4 pages
   constexpr int CHUNKS = D / 8;                  // 16-byte chunks per key row
-  constexpr int PIECES = KT * CHUNKS / kThreads; // chunks per thread per tensor per tile
+  constexpr int ROWB = D * 2;                    // bytes per key row in LDS
+  constexpr int RPR = 1024 / ROWB;               // key rows per 1 KiB wave load
+  constexpr int NREG = KT * ROWB / 1024 / kExtWaves;  // 1 KiB loads per wave per tensor
   constexpr int KSTEPS = D / 16;                 // MFMA k-steps of the score product
   constexpr int DT = D / 32;                     // 32-wide output column tiles
   constexpr int TILE_ELEMS = KT * D;
-  __shared__ __attribute__((aligned(16))) __bf16 smem[2 * 2 * TILE_ELEMS];  // [buf][K|V][key][D]
+  constexpr bool kDirect = sizeof(T) == 2;       // bf16 storage: global -> LDS directly
+  constexpr float kRescaleSlack = 8.0f;          // log2 headroom before O is rescaled
+  __shared__ __attribute__((aligned(1024))) KvTile<D> tile0;
+  __shared__ __attribute__((aligned(1024))) KvTile<D> tile1;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int hh = lane >> 5;     // lane half
   const int l32 = lane & 31;
 
@@ -129,6 +144,7 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
   const int r0 = rt * kExtTileRows;
   const int P = sd.prefix;
   const int L = P + sd.suffix;
+  const int nblk = (L + kBlock - 1) / kBlock;
 
   // keys this tile needs: up to the last query's own position
   const int t_last = min(sd.suffix - 1, (r0 + kExtTileRows - 1) / G);
@@ -155,81 +171,91 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
 
   const T* kpool = reinterpret_cast<const T*>(a.k_pool);
   const T* vpool = reinterpret_cast<const T*>(a.v_pool);
-  const int32_t* bt = a.block_table + (int64_t)sd.seq * a.max_blocks;
+  // the block table is read-only here: a constant-address-space view lets
+  // wave-uniform page lookups become scalar loads
+  const __attribute__((address_space(4))) int32_t* bt =
+      (const __attribute__((address_space(4))) int32_t*)(a.block_table + (int64_t)sd.seq * a.max_blocks);
+  const uint32_t nb_max = (uint32_t)min<int64_t>(a.num_blocks, 0x7fffffff) - 1u;
 
-  // ---- global -> register staging of one K/V tile
-  u32x4 stK[PIECES], stV[PIECES];
-  auto fetch = [&](int j) {
+  // ---- gather geometry: wave `wave`, load i covers key rows RPR*(wave+8i) ..
+  // +RPR-1 of the tile, all inside one page.  Lane l lands at LDS byte
+  // 16*l of that 1 KiB run, i.e. row RPR*(wave+8i) + l/CHUNKS, physical chunk
+  // l%CHUNKS, so it fetches logical chunk (l%CHUNKS) ^ swizzle(row).
+  int keyrow[NREG], lds_off[NREG], chunk_off[NREG], page_in_tile[NREG];
 #pragma unroll
-    for (int i = 0; i < PIECES; ++i) {
-      const int p = tid + i * kThreads;
-      const int key = p / CHUNKS;
-      const int cl = p % CHUNKS;
-      const int kabs = j * KT + key;
-      u32x4 kv = {0u, 0u, 0u, 0u}, vv = {0u, 0u, 0u, 0u};
-      if (kabs < L) {
-        const int bid = bt[kabs / kBlock];
-        if (bid >= 0 && (int64_t)bid < a.num_blocks) {
-          const int64_t off = ((((int64_t)bid * hkv + g) * kBlock) + (kabs % kBlock)) * D + cl * 8;
-          kv = load8(kpool + off);
-          vv = load8(vpool + off);
-        }
-      }
-      stK[i] = kv;
-      stV[i] = vv;
+  for (int i = 0; i < NREG; ++i) {
+    const int run = wave + kExtWaves * i;
+    keyrow[i] = RPR * run + lane / CHUNKS;
+    page_in_tile[i] = (RPR * run) / kBlock;
+    lds_off[i] = run * 512;                                   // elements
+    chunk_off[i] = (((lane % CHUNKS) ^ swz<D>(keyrow[i])) << 3);
+  }
+  // physical page ids of the pages a tile needs (wave-uniform, clamped into the pool)
+  auto page_ids = [&](int jn, uint32_t (&ids)[NREG]) {
+#pragma unroll
+    for (int i = 0; i < NREG; ++i) {
+      const int page = __builtin_amdgcn_readfirstlane(min(jn * 4 + page_in_tile[i], nblk - 1));
+      const uint32_t raw = (uint32_t)bt[page];
+      ids[i] = __builtin_amdgcn_readfirstlane(raw > nb_max ? nb_max : raw);
     }
   };
-  auto stash = [&](int buf) {
-    __bf16* ks = smem + buf * 2 * TILE_ELEMS;
-    __bf16* vs = ks + TILE_ELEMS;
+  // element offset of this lane's chunk; positions past the end of the
+  // sequence read the last real position instead (finite data whose weight is 0)
+  auto src_off = [&](int jn, int i, uint32_t id) -> int64_t {
+    const int page = min(jn * 4 + page_in_tile[i], nblk - 1);
+    const int last = L - 1 - page * kBlock;
+    const int slot = min(keyrow[i] & (kBlock - 1), last);
+    return ((((int64_t)id * hkv + g) << 4) + slot) * D + chunk_off[i];
+  };
+  u32x4 stK[NREG], stV[NREG];   // register staging (fp32 storage only)
+  auto issue = [&](int jn, const uint32_t (&ids)[NREG], KvTile<D>& dst) {
 #pragma unroll
-    for (int i = 0; i < PIECES; ++i) {
-      const int p = tid + i * kThreads;
-      const int key = p / CHUNKS;
-      const int cl = p % CHUNKS;
-      const int o = key * D + ((cl ^ swz<D>(key)) << 3);
-      *reinterpret_cast<u32x4*>(ks + o) = stK[i];
-      *reinterpret_cast<u32x4*>(vs + o) = stV[i];
+    for (int i = 0; i < NREG; ++i) {
+      const int64_t off = src_off(jn, i, ids[i]);
+      if constexpr (kDirect) {
+        lds_bf16* kd = (lds_bf16*)dst.kv + lds_off[i];
+        __builtin_amdgcn_global_load_lds((const void*)(kpool + off), (__attribute__((address_space(3))) void*)kd, 16, 0, 0);
+        __builtin_amdgcn_global_load_lds((const void*)(vpool + off), (__attribute__((address_space(3))) void*)(kd + TILE_ELEMS), 16, 0, 0);
+      } else {
+        stK[i] = load8(kpool + off);
+        stV[i] = load8(vpool + off);
+      }
+    }
+  };
+  auto stash = [&](KvTile<D>& dst) {
+    if constexpr (!kDirect) {
+#pragma unroll
+      for (int i = 0; i < NREG; ++i) {
+        *reinterpret_cast<u32x4*>(dst.kv + lds_off[i] + lane * 8) = stK[i];
+        *reinterpret_cast<u32x4*>(dst.kv + TILE_ELEMS + lds_off[i] + lane * 8) = stV[i];
+      }
     }
   };
 
   f32x16 o[DT];
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt) o[dt] = (f32x16){};
-  float m_run = -INFINITY;   // running max of scale*log2e*score
-  float l_run = 0.f;         // this lane's share of the running row sum
+  float m_ref = -INFINITY;   // reference max of scale*log2e*score (may trail the true max by < 8)
+  float l_run = 0.f;         // this lane's share of sum 2^(s*c - m_ref)
   const float c = a.scale_log2;
+  const int g16 = (lane >> 4) & 1;
+  const int rsel = (lane & 15) >> 2;
 
-  if (j0 < j1) {
-    fetch(j0);
-    stash(0);
-  }
-  __syncthreads();
-
-  for (int j = j0; j < j1; ++j) {
-    const int buf = (j - j0) & 1;
-    if (j + 1 < j1) fetch(j + 1);
-    const __bf16* ks = smem + buf * 2 * TILE_ELEMS;
-    const __bf16* vs = ks + TILE_ELEMS;
-
-    // ---- S^T = K Q^T for two 32-key halves
-    f32x16 s[2];
+  auto compute = [&](int j, const KvTile<D>& tl) {
+    const __bf16* ks = tl.kv;
+    const __bf16* vs = tl.kv + TILE_ELEMS;
+    // ---- S^T = K Q^T, two independent 32-key chains interleaved
+    f32x16 s[2] = {{}, {}};
+    const int sw0 = swz<D>(l32), sw1 = swz<D>(32 + l32);
 #pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      const int key = half * 32 + l32;
-      const __bf16* krow = ks + key * D;
-      const int sw = swz<D>(key);
-      f32x16 acc = {};
-#pragma unroll
-      for (int kk = 0; kk < KSTEPS; ++kk) {
-        const int cl = 2 * kk + hh;
-        const bf16x8 kf = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(krow + ((cl ^ sw) << 3)));
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qreg[kk], acc, 0, 0, 0);
-      }
-      s[half] = acc;
+    for (int kk = 0; kk < KSTEPS; ++kk) {
+      const int cl = 2 * kk + hh;
+      const bf16x8 k0 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(ks + l32 * D + ((cl ^ sw0) << 3)));
+      const bf16x8 k1 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(ks + (32 + l32) * D + ((cl ^ sw1) << 3)));
+      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qreg[kk], s[0], 0, 0, 0);
+      s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qreg[kk], s[1], 0, 0, 0);
     }
-
-    // ---- causal mask (only tiles that reach past the tile's first query)
+    // ---- causal mask: only tiles that reach past the tile's first query
     if (j * KT + KT - 1 > lim_min) {
 #pragma unroll
       for (int half = 0; half < 2; ++half)
@@ -239,18 +265,24 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
           if (kabs > lim) s[half][e] = -INFINITY;
         }
     }
-
-    // ---- online softmax (log2 domain)
+    // ---- online softmax (log2 domain); O and l are rescaled only when the
+    // tile max passes the reference by more than the slack
     float mx = -INFINITY;
 #pragma unroll
     for (int half = 0; half < 2; ++half)
 #pragma unroll
       for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[half][e]);
-    mx = pair_max(mx);
-    const float m_new = fmaxf(m_run, mx * c);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-    m_run = m_new;
+    const float mxc = pair_max(mx) * c;
+    const bool up = mxc > m_ref + kRescaleSlack;
+    if (__builtin_amdgcn_ballot_w64(up) != 0) {
+      const float m_new = up ? mxc : m_ref;
+      const float alpha = __builtin_amdgcn_exp2f(m_ref - m_new);   // 1 where unchanged, 0 from -inf
+      m_ref = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
+    }
+    const float m_use = (m_ref == -INFINITY) ? 0.f : m_ref;
     float rs = 0.f;
 #pragma unroll
     for (int half = 0; half < 2; ++half)
@@ -260,44 +292,67 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
         s[half][e] = p;
         rs += p;
       }
-    l_run = l_run * alpha + rs;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
-
+    l_run += rs;
     // ---- P^T as the B operand: key group kg = 16 keys = 8 accumulators
     bf16x8 pb[4];
 #pragma unroll
     for (int kg = 0; kg < 4; ++kg) {
       const f32x16& sv = s[kg >> 1];
       const int b0 = (kg & 1) * 8;
-      u32x4 w;
+      u32x4 wv;
 #pragma unroll
       for (int q2 = 0; q2 < 4; ++q2)
-        w[q2] = __builtin_bit_cast(unsigned, __builtin_convertvector((f32x2){sv[b0 + 2 * q2], sv[b0 + 2 * q2 + 1]}, bf16x2));
-      pb[kg] = __builtin_bit_cast(bf16x8, w);
+        wv[q2] = __builtin_bit_cast(unsigned, __builtin_convertvector((f32x2){sv[b0 + 2 * q2], sv[b0 + 2 * q2 + 1]}, bf16x2));
+      pb[kg] = __builtin_bit_cast(bf16x8, wv);
     }
-
     // ---- O^T += V^T P^T; V^T from the row-major tile by transposed reads
-    const int g16 = (lane >> 4) & 1;
-    const int rsel = (lane & 15) >> 2;
+    const lds_bf16* vl = (const lds_bf16*)vs;
 #pragma unroll
     for (int kg = 0; kg < 4; ++kg) {
       const int key1 = kg * 16 + 4 * hh + rsel;
       const int key2 = key1 + 8;
-      const int sw1 = swz<D>(key1), sw2 = swz<D>(key2);
+      const int sw1k = swz<D>(key1), sw2k = swz<D>(key2);
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
         const int dcol = dt * 32 + g16 * 16 + 4 * (lane & 3);
-        const int o1 = key1 * D + (((dcol >> 3) ^ sw1) << 3) + (dcol & 7);
-        const int o2 = key2 * D + (((dcol >> 3) ^ sw2) << 3) + (dcol & 7);
-        const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)((__attribute__((address_space(3))) __bf16*)smem + (vs - smem) + o1));
-        const bf16x4 v2 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)((__attribute__((address_space(3))) __bf16*)smem + (vs - smem) + o2));
+        const int o1 = key1 * D + (((dcol >> 3) ^ sw1k) << 3) + (dcol & 7);
+        const int o2 = key2 * D + (((dcol >> 3) ^ sw2k) << 3) + (dcol & 7);
+        const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vl + o1));
+        const bf16x4 v2 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vl + o2));
         const bf16x8 vf = __builtin_shufflevector(v1, v2, 0, 1, 2, 3, 4, 5, 6, 7);
         o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[kg], o[dt], 0, 0, 0);
       }
     }
+  };
 
-    if (j + 1 < j1) stash(buf ^ 1);
+  // ---- pipeline: tile j is computed from one buffer while tile j+1 streams
+  // into the other; page ids run two tiles ahead.
+  uint32_t ids[NREG];
+  page_ids(j0, ids);
+  if (j0 < j1) {
+    issue(j0, ids, tile0);
+    stash(tile0);
+  }
+  page_ids(j0 + 1, ids);
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+  __syncthreads();
+  for (int j = j0; j < j1; j += 2) {
+    if (j + 1 < j1) {
+      issue(j + 1, ids, tile1);
+      page_ids(j + 2, ids);
+    }
+    compute(j, tile0);
+    if (j + 1 < j1) stash(tile1);
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    __syncthreads();
+    if (j + 1 >= j1) break;
+    if (j + 2 < j1) {
+      issue(j + 2, ids, tile0);
+      page_ids(j + 3, ids);
+    }
+    compute(j + 1, tile1);
+    if (j + 2 < j1) stash(tile0);
+    __builtin_amdgcn_s_waitcnt(0x0F70);
     __syncthreads();
   }
 
@@ -314,7 +369,7 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
         const int d = dt * 32 + 8 * i + 4 * hh;
         store4(op + d, o[dt][4 * i] * inv, o[dt][4 * i + 1] * inv, o[dt][4 * i + 2] * inv, o[dt][4 * i + 3] * inv);
       }
-    if (a.lse != nullptr && hh == 0) a.lse[qrow] = (m_run + __builtin_log2f(l_tot)) * kLn2;
+    if (a.lse != nullptr && hh == 0) a.lse[qrow] = (m_ref + __builtin_log2f(l_tot)) * kLn2;
   } else {
     const int64_t prow = (int64_t)split * a.total_rows * a.num_q_heads + qrow;
     float* op = a.part_o + prow * D;
@@ -326,7 +381,7 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
         store4(op + d, o[dt][4 * i], o[dt][4 * i + 1], o[dt][4 * i + 2], o[dt][4 * i + 3]);
       }
     if (hh == 0) {
-      a.part_ml[prow * 2] = m_run;
+      a.part_ml[prow * 2] = m_ref;
       a.part_ml[prow * 2 + 1] = l_tot;
     }
   }

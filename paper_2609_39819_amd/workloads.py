@@ -48,8 +48,12 @@ def f32_to_bf16_bits(x: np.ndarray, chunk: int = 1 << 24) -> np.ndarray:
     flat = x.reshape(-1)
     out = np.empty(flat.shape, dtype=np.uint16)
     for s in range(0, flat.size, chunk):
-        u = flat[s:s + chunk].view(np.uint32).astype(np.uint64)
-        r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+        u = flat[s:s + chunk].view(np.uint32)
+        # u + 0x7FFF + lsb only wraps for NaN bit patterns, which are replaced below
+        r = u + np.uint32(0x7FFF)
+        r += (u >> 16) & np.uint32(1)
+        r >>= 16
+        r = r.astype(np.uint16)
         nan = np.isnan(flat[s:s + chunk])
         if nan.any():
             r[nan] = BF16_NAN
