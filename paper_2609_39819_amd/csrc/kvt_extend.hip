@@ -6,20 +6,22 @@
 //   * one kv-head g and 256 packed query rows (row r = token r/G, head
 //     g*G + r%G): the G query heads that share a kv-head share every K/V
 //     tile staged in LDS;
-//   * 8 waves, each owning 32 rows; the wave computes S^T = K Q^T with
-//     v_mfma_f32_32x32x16_bf16 (keys on the MFMA rows, queries on the
-//     columns), so a query's scores sit in one lane pair (l, l+32) and the
-//     row max / row sum need a single permlane32 swap;
+//   * 8 waves (two per SIMD), each owning 32 rows; the wave computes
+//     S^T = K Q^T with v_mfma_f32_32x32x16_bf16 (keys on the MFMA rows,
+//     queries on the columns), so a query's scores sit in one lane pair
+//     (l, l+32) and the row max / row sum need a single permlane32 swap;
 //   * the probabilities leave the S^T accumulators already in the B-operand
 //     layout of O^T += V^T P^T; the V^T operand comes straight from the
 //     row-major V tile through ds_read_b64_tr_b16;
 //   * fp32 online softmax in log2 units (scale*log2e folded into one FMA);
 //   * K/V tiles of 64 keys (4 pages) are gathered through the block table
-//     into a double-buffered LDS ring; every page contributes one contiguous
-//     run of 16*D elements per kv-head, read with 16-byte coalesced loads.
+//     straight into a double-buffered LDS ring (global_load_lds_dwordx4);
+//     every page contributes one contiguous run of 16*D elements per
+//     kv-head, read with 16-byte coalesced loads; the next tile streams in
+//     while the current one is computed.
 // Positions past the end of the sequence and unused page slots are never
-// multiplied in: their K/V are replaced by zeros in LDS and their scores by
-// -inf.
+// multiplied in: their loads read the last real position instead (finite
+// data) and their scores are replaced by -inf, so their weight is exactly 0.
 #include "kvt_internal.h"
 
 namespace kvt {
@@ -38,14 +40,17 @@ typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
 constexpr float kLn2 = 0.693147180559945309f;
 constexpr int kThreads = kExtWaves * 64;
 
-// XOR swizzle of the 16-byte chunks of one key row in LDS.  Over any 8
-// consecutive keys the K-operand reads (one chunk column, 8 rows) hit 8
-// distinct bank groups, and over any 4 consecutive keys the transposed V
-// reads (two adjacent chunks, 4 rows) do too.
+// XOR swizzle of the 16-byte chunks of one key row in LDS (64 banks of 4 B,
+// so 256 B per bank cycle).  D = 128 (16 chunks per 256-B row):
+// s = (key&3)<<2 | (key>>2)&3 is a bijection on key%16, so the K-operand
+// reads (16 lanes, 16 consecutive keys, one chunk column) hit 16 distinct
+// bank groups, and the transposed V reads (32 lanes: 4 consecutive keys x 4
+// adjacent chunks) do too.  D = 64 (8 chunks per 128-B row, two rows per bank
+// cycle): s = ((key>>1)&1)<<2 | (key>>2)&3 gives the same two properties.
 template <int D>
 __device__ __forceinline__ int swz(int key) {
-  const int s = ((key & 3) << 1) | ((key >> 2) & 1) | (((key >> 3) & 1) << 3);
-  return D == 128 ? s : (s & 7);
+  if constexpr (D == 128) return ((key & 3) << 2) | ((key >> 2) & 3);
+  else return (((key >> 1) & 1) << 2) | ((key >> 2) & 3);
 }
 
 // 8 consecutive elements as bf16 (fp32 storage is rounded to nearest even).
@@ -99,12 +104,19 @@ __device__ __forceinline__ float pair_sum(float x) {
 
 typedef __attribute__((address_space(3))) __bf16 lds_bf16;
 
-// One K/V tile of 64 keys in LDS: [K|V][key][D] bf16, 16-byte chunks of each
-// key row XOR-swizzled.  Two tiles form the double buffer; they are distinct
-// objects so the compiler can tell loads into one from reads of the other.
+// One K or V tile of 64 keys in LDS: [key][D] bf16, the 16-byte chunks of
+// each key row XOR-swizzled.  A ring slot is one object holding K then V, so
+// every operand read of a slot is a per-lane offset plus an immediate; the
+// two slots are distinct objects so the compiler can tell the page gather
+// into one slot from the operand reads of the other.
 template <int D>
-struct KvTile {
-  __bf16 kv[2 * kExtKeysPerTile * D];
+struct HalfTile {
+  __bf16 e[kExtKeysPerTile * D];
+};
+template <int D>
+struct Slot {
+  HalfTile<D>& k;
+  HalfTile<D>& v;
 };
 
 template <typename T, int D>
@@ -116,11 +128,12 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
   constexpr int NREG = KT * ROWB / 1024 / kExtWaves;  // 1 KiB loads per wave per tensor
   constexpr int KSTEPS = D / 16;                 // MFMA k-steps of the score product
   constexpr int DT = D / 32;                     // 32-wide output column tiles
-  constexpr int TILE_ELEMS = KT * D;
   constexpr bool kDirect = sizeof(T) == 2;       // bf16 storage: global -> LDS directly
   constexpr float kRescaleSlack = 8.0f;          // log2 headroom before O is rescaled
-  __shared__ __attribute__((aligned(1024))) KvTile<D> tile0;
-  __shared__ __attribute__((aligned(1024))) KvTile<D> tile1;
+  constexpr int NB = kExtRowsPerWave / 32;       // 32-row MFMA blocks per wave
+  __shared__ __attribute__((aligned(1024))) HalfTile<D> slot0[2];   // K, V
+  __shared__ __attribute__((aligned(1024))) HalfTile<D> slot1[2];
+  const Slot<D> tile0{slot0[0], slot0[1]}, tile1{slot1[0], slot1[1]};
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -155,19 +168,27 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
   const int j1 = min(ntiles_kv, j0 + per_split);
   const int lim_min = P + r0 / G;   // smallest causal limit of the tile
 
-  // ---- this lane's query row
-  int r = r0 + wave * kExtRowsPerWave + l32;
-  const bool row_valid = r < rows_seq;
-  if (!row_valid) r = rows_seq - 1;
-  const int t = r / G;
-  const int h = g * G + (r - t * G);
-  const int lim = P + t;                               // last visible position
-  const int64_t qrow = (int64_t)(sd.row_off + t) * a.num_q_heads + h;
-
-  const T* qp = reinterpret_cast<const T*>(a.q) + qrow * D;
-  bf16x8 qreg[KSTEPS];
+  // ---- this lane's query rows: block b = rows kExtRowsPerWave*wave + 32*b + l32
+  int lim[NB];
+  bool row_valid[NB];
+  int64_t qrow[NB];
 #pragma unroll
-  for (int kk = 0; kk < KSTEPS; ++kk) qreg[kk] = __builtin_bit_cast(bf16x8, load8(qp + kk * 16 + hh * 8));
+  for (int b = 0; b < NB; ++b) {
+    int r = r0 + wave * kExtRowsPerWave + b * 32 + l32;
+    row_valid[b] = r < rows_seq;
+    if (!row_valid[b]) r = rows_seq - 1;
+    const int t = r / G;
+    const int h = g * G + (r - t * G);
+    lim[b] = P + t;                                     // last visible position
+    qrow[b] = (int64_t)(sd.row_off + t) * a.num_q_heads + h;
+  }
+  bf16x8 qreg[NB][KSTEPS];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    const T* qp = reinterpret_cast<const T*>(a.q) + qrow[b] * D;
+#pragma unroll
+    for (int kk = 0; kk < KSTEPS; ++kk) qreg[b][kk] = __builtin_bit_cast(bf16x8, load8(qp + kk * 16 + hh * 8));
+  }
 
   const T* kpool = reinterpret_cast<const T*>(a.k_pool);
   const T* vpool = reinterpret_cast<const T*>(a.v_pool);
@@ -177,9 +198,9 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
       (const __attribute__((address_space(4))) int32_t*)(a.block_table + (int64_t)sd.seq * a.max_blocks);
   const uint32_t nb_max = (uint32_t)min<int64_t>(a.num_blocks, 0x7fffffff) - 1u;
 
-  // ---- gather geometry: wave `wave`, load i covers key rows RPR*(wave+8i) ..
+  // ---- gather geometry: wave w, load i covers key rows RPR*(w + 8i) ..
   // +RPR-1 of the tile, all inside one page.  Lane l lands at LDS byte
-  // 16*l of that 1 KiB run, i.e. row RPR*(wave+8i) + l/CHUNKS, physical chunk
+  // 16*l of that 1 KiB run, i.e. row RPR*(w + 8i) + l/CHUNKS, physical chunk
   // l%CHUNKS, so it fetches logical chunk (l%CHUNKS) ^ swizzle(row).
   int keyrow[NREG], lds_off[NREG], chunk_off[NREG], page_in_tile[NREG];
 #pragma unroll
@@ -191,7 +212,7 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
     chunk_off[i] = (((lane % CHUNKS) ^ swz<D>(keyrow[i])) << 3);
   }
   // physical page ids of the pages a tile needs (wave-uniform, clamped into the pool)
-  auto page_ids = [&](int jn, uint32_t (&ids)[NREG]) {
+  auto page_ids = [&](int jn, uint32_t (&ids)[NREG]) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < NREG; ++i) {
       const int page = __builtin_amdgcn_readfirstlane(min(jn * 4 + page_in_tile[i], nblk - 1));
@@ -201,188 +222,229 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
   };
   // element offset of this lane's chunk; positions past the end of the
   // sequence read the last real position instead (finite data whose weight is 0)
-  auto src_off = [&](int jn, int i, uint32_t id) -> int64_t {
+  auto src_off = [&](int jn, int i, uint32_t id) __attribute__((always_inline)) -> int64_t {
     const int page = min(jn * 4 + page_in_tile[i], nblk - 1);
     const int last = L - 1 - page * kBlock;
     const int slot = min(keyrow[i] & (kBlock - 1), last);
     return ((((int64_t)id * hkv + g) << 4) + slot) * D + chunk_off[i];
   };
   u32x4 stK[NREG], stV[NREG];   // register staging (fp32 storage only)
-  auto issue = [&](int jn, const uint32_t (&ids)[NREG], KvTile<D>& dst) {
+  auto issue = [&](int jn, const uint32_t (&ids)[NREG], const Slot<D>& dst) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < NREG; ++i) {
       const int64_t off = src_off(jn, i, ids[i]);
       if constexpr (kDirect) {
-        lds_bf16* kd = (lds_bf16*)dst.kv + lds_off[i];
+        lds_bf16* kd = (lds_bf16*)dst.k.e + lds_off[i];
+        lds_bf16* vd = (lds_bf16*)dst.v.e + lds_off[i];
         __builtin_amdgcn_global_load_lds((const void*)(kpool + off), (__attribute__((address_space(3))) void*)kd, 16, 0, 0);
-        __builtin_amdgcn_global_load_lds((const void*)(vpool + off), (__attribute__((address_space(3))) void*)(kd + TILE_ELEMS), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds((const void*)(vpool + off), (__attribute__((address_space(3))) void*)vd, 16, 0, 0);
       } else {
         stK[i] = load8(kpool + off);
         stV[i] = load8(vpool + off);
       }
     }
   };
-  auto stash = [&](KvTile<D>& dst) {
+  auto stash = [&](const Slot<D>& dst) __attribute__((always_inline)) {
     if constexpr (!kDirect) {
 #pragma unroll
       for (int i = 0; i < NREG; ++i) {
-        *reinterpret_cast<u32x4*>(dst.kv + lds_off[i] + lane * 8) = stK[i];
-        *reinterpret_cast<u32x4*>(dst.kv + TILE_ELEMS + lds_off[i] + lane * 8) = stV[i];
+        *reinterpret_cast<u32x4*>(dst.k.e + lds_off[i] + lane * 8) = stK[i];
+        *reinterpret_cast<u32x4*>(dst.v.e + lds_off[i] + lane * 8) = stV[i];
       }
     }
   };
 
-  f32x16 o[DT];
+  f32x16 o[NB][DT];
 #pragma unroll
-  for (int dt = 0; dt < DT; ++dt) o[dt] = (f32x16){};
-  float m_ref = -INFINITY;   // reference max of scale*log2e*score (may trail the true max by < 8)
-  float l_run = 0.f;         // this lane's share of sum 2^(s*c - m_ref)
+  for (int b = 0; b < NB; ++b)
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) o[b][dt] = (f32x16){};
+  // m_ref: reference max of scale*log2e*score (trails the true max by less
+  // than the slack); l_run: this lane's share of sum 2^(s*c - m_ref)
+  float m_ref[NB], l_run[NB];
+#pragma unroll
+  for (int b = 0; b < NB; ++b) m_ref[b] = -INFINITY, l_run[b] = 0.f;
   const float c = a.scale_log2;
   const int g16 = (lane >> 4) & 1;
   const int rsel = (lane & 15) >> 2;
 
-  auto compute = [&](int j, const KvTile<D>& tl) {
-    const __bf16* ks = tl.kv;
-    const __bf16* vs = tl.kv + TILE_ELEMS;
-    // ---- S^T = K Q^T, two independent 32-key chains interleaved
-    f32x16 s[2] = {{}, {}};
-    const int sw0 = swz<D>(l32), sw1 = swz<D>(32 + l32);
+  // lane-constant LDS element offsets of the MFMA operand reads; the 32-key
+  // half and 16-key group parts are compile-time constants
+  int koff[KSTEPS], voff[DT][2];
+#pragma unroll
+  for (int kk = 0; kk < KSTEPS; ++kk) koff[kk] = l32 * D + (((2 * kk + hh) ^ swz<D>(l32)) << 3);
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+    for (int r2 = 0; r2 < 2; ++r2) {
+      const int key = 8 * r2 + 4 * hh + rsel;          // key within a 16-key group
+      const int dcol = dt * 32 + g16 * 16 + 4 * (lane & 3);
+      voff[dt][r2] = key * D + (((dcol >> 3) ^ swz<D>(key)) << 3) + (dcol & 7);
+    }
+  // ---- S^T = K Q^T of one tile: two independent 32-key accumulator chains
+  // per 32-row block, each K fragment read from LDS feeding NB blocks
+  auto qk = [&](const Slot<D>& tl, f32x16 (&s)[NB][2]) __attribute__((always_inline)) {
+    const __bf16* ks = tl.k.e;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) s[b][0] = s[b][1] = (f32x16){};
 #pragma unroll
     for (int kk = 0; kk < KSTEPS; ++kk) {
-      const int cl = 2 * kk + hh;
-      const bf16x8 k0 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(ks + l32 * D + ((cl ^ sw0) << 3)));
-      const bf16x8 k1 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(ks + (32 + l32) * D + ((cl ^ sw1) << 3)));
-      s[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qreg[kk], s[0], 0, 0, 0);
-      s[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qreg[kk], s[1], 0, 0, 0);
+      const bf16x8 k0 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(ks + koff[kk]));
+      const bf16x8 k1 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(ks + koff[kk] + 32 * D));
+#pragma unroll
+      for (int b = 0; b < NB; ++b) {
+        s[b][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qreg[b][kk], s[b][0], 0, 0, 0);
+        s[b][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qreg[b][kk], s[b][1], 0, 0, 0);
+      }
     }
-    // ---- causal mask: only tiles that reach past the tile's first query
+  };
+  // ---- between tiles: causal mask of tile j (only tiles reaching past the
+  // tile's first query), row max, and the reference-max update.  The
+  // reference only moves when a tile max passes it by more than the slack;
+  // O and l are then rescaled (rare after the first tiles).
+  auto settle = [&](int j, f32x16 (&s)[NB][2]) __attribute__((always_inline)) {
     if (j * KT + KT - 1 > lim_min) {
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int half = 0; half < 2; ++half)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int kabs = j * KT + half * 32 + 8 * (e >> 2) + 4 * hh + (e & 3);
+            if (kabs > lim[b]) s[b][half][e] = -INFINITY;
+          }
+    }
+    float alpha[NB];
+    bool moved = false;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      float mx = -INFINITY;
 #pragma unroll
       for (int half = 0; half < 2; ++half)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int kabs = j * KT + half * 32 + 8 * (e >> 2) + 4 * hh + (e & 3);
-          if (kabs > lim) s[half][e] = -INFINITY;
+        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[b][half][e]);
+      const float mxc = pair_max(mx) * c;
+      const float m_new = (mxc > m_ref[b] + kRescaleSlack) ? mxc : m_ref[b];
+      alpha[b] = __builtin_amdgcn_exp2f(m_ref[b] - m_new);   // 1 when unchanged, 0 from -inf
+      m_ref[b] = m_new;
+      l_run[b] *= alpha[b];
+      moved = moved || alpha[b] != 1.0f;
+    }
+    if (__builtin_amdgcn_ballot_w64(moved) != 0) {
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) o[b][dt] *= alpha[b];
+    }
+  };
+  // ---- probabilities of a settled tile: P^T as the B operand of the value
+  // product (key group kg = 16 keys); the row sum adds the bf16 values the
+  // value product uses
+  auto probs = [&](f32x16 (&s)[NB][2], bf16x8 (&pb)[NB][4]) __attribute__((always_inline)) {
+    const bf16x2 ones = {(__bf16)1.0f, (__bf16)1.0f};
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const float m_use = (m_ref[b] == -INFINITY) ? 0.f : m_ref[b];
+      float rs = 0.f;
+#pragma unroll
+      for (int kg = 0; kg < 4; ++kg) {
+        const int half = kg >> 1, b0 = (kg & 1) * 8;
+        u32x4 wv;
+#pragma unroll
+        for (int q2 = 0; q2 < 4; ++q2) {
+          const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[b][half][b0 + 2 * q2], c, -m_use));
+          const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[b][half][b0 + 2 * q2 + 1], c, -m_use));
+          const bf16x2 pp = __builtin_convertvector((f32x2){p0, p1}, bf16x2);
+          rs = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, rs, false);
+          wv[q2] = __builtin_bit_cast(unsigned, pp);
         }
-    }
-    // ---- online softmax (log2 domain); O and l are rescaled only when the
-    // tile max passes the reference by more than the slack
-    float mx = -INFINITY;
-#pragma unroll
-    for (int half = 0; half < 2; ++half)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[half][e]);
-    const float mxc = pair_max(mx) * c;
-    const bool up = mxc > m_ref + kRescaleSlack;
-    if (__builtin_amdgcn_ballot_w64(up) != 0) {
-      const float m_new = up ? mxc : m_ref;
-      const float alpha = __builtin_amdgcn_exp2f(m_ref - m_new);   // 1 where unchanged, 0 from -inf
-      m_ref = m_new;
-      l_run *= alpha;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) o[dt] *= alpha;
-    }
-    const float m_use = (m_ref == -INFINITY) ? 0.f : m_ref;
-    float rs = 0.f;
-#pragma unroll
-    for (int half = 0; half < 2; ++half)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[half][e], c, -m_use));
-        s[half][e] = p;
-        rs += p;
+        pb[b][kg] = __builtin_bit_cast(bf16x8, wv);
       }
-    l_run += rs;
-    // ---- P^T as the B operand: key group kg = 16 keys = 8 accumulators
-    bf16x8 pb[4];
-#pragma unroll
-    for (int kg = 0; kg < 4; ++kg) {
-      const f32x16& sv = s[kg >> 1];
-      const int b0 = (kg & 1) * 8;
-      u32x4 wv;
-#pragma unroll
-      for (int q2 = 0; q2 < 4; ++q2)
-        wv[q2] = __builtin_bit_cast(unsigned, __builtin_convertvector((f32x2){sv[b0 + 2 * q2], sv[b0 + 2 * q2 + 1]}, bf16x2));
-      pb[kg] = __builtin_bit_cast(bf16x8, wv);
+      l_run[b] += rs;
     }
-    // ---- O^T += V^T P^T; V^T from the row-major tile by transposed reads
-    const lds_bf16* vl = (const lds_bf16*)vs;
+  };
+  // ---- O^T += V^T P^T; V^T comes from the row-major tile by transposed
+  // reads, each fragment feeding NB MFMAs
+  auto pv = [&](const Slot<D>& tl, const bf16x8 (&pb)[NB][4]) __attribute__((always_inline)) {
+    const lds_bf16* vl = (const lds_bf16*)tl.v.e;
 #pragma unroll
     for (int kg = 0; kg < 4; ++kg) {
-      const int key1 = kg * 16 + 4 * hh + rsel;
-      const int key2 = key1 + 8;
-      const int sw1k = swz<D>(key1), sw2k = swz<D>(key2);
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        const int dcol = dt * 32 + g16 * 16 + 4 * (lane & 3);
-        const int o1 = key1 * D + (((dcol >> 3) ^ sw1k) << 3) + (dcol & 7);
-        const int o2 = key2 * D + (((dcol >> 3) ^ sw2k) << 3) + (dcol & 7);
-        const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vl + o1));
-        const bf16x4 v2 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vl + o2));
+        const bf16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vl + voff[dt][0] + kg * 16 * D));
+        const bf16x4 v2 = __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4*)(vl + voff[dt][1] + kg * 16 * D));
         const bf16x8 vf = __builtin_shufflevector(v1, v2, 0, 1, 2, 3, 4, 5, 6, 7);
-        o[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[kg], o[dt], 0, 0, 0);
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+          o[b][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[b][kg], o[b][dt], 0, 0, 0);
       }
     }
   };
 
-  // ---- pipeline: tile j is computed from one buffer while tile j+1 streams
-  // into the other; page ids run two tiles ahead.
+  // ---- main loop.  Step t first starts the gather of tile t+1 into the
+  // other slot (its page ids were fetched a step earlier), then computes
+  // tile t: scores, settle, probabilities, value product.  The wait + barrier
+  // at the end publishes tile t+1 and frees the slot of tile t for the
+  // gather of tile t+2.
+  const int n = j1 - j0;
   uint32_t ids[NREG];
   page_ids(j0, ids);
-  if (j0 < j1) {
-    issue(j0, ids, tile0);
-    stash(tile0);
-  }
+  if (n > 0) { issue(j0, ids, tile0); stash(tile0); }
   page_ids(j0 + 1, ids);
   __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
   __syncthreads();
-  for (int j = j0; j < j1; j += 2) {
-    if (j + 1 < j1) {
-      issue(j + 1, ids, tile1);
-      page_ids(j + 2, ids);
+  f32x16 s_cur[NB][2];
+  bf16x8 pb[NB][4];
+  auto step = [&](int t, const Slot<D>& cur, const Slot<D>& fill) __attribute__((always_inline)) {
+    if (t + 1 < n) {
+      issue(j0 + t + 1, ids, fill);
+      stash(fill);
+      page_ids(j0 + t + 2, ids);
     }
-    compute(j, tile0);
-    if (j + 1 < j1) stash(tile1);
+    qk(cur, s_cur);
+    settle(j0 + t, s_cur);
+    probs(s_cur, pb);
+    pv(cur, pb);
     __builtin_amdgcn_s_waitcnt(0x0F70);
     __syncthreads();
-    if (j + 1 >= j1) break;
-    if (j + 2 < j1) {
-      issue(j + 2, ids, tile0);
-      page_ids(j + 3, ids);
-    }
-    compute(j + 1, tile1);
-    if (j + 2 < j1) stash(tile0);
-    __builtin_amdgcn_s_waitcnt(0x0F70);
-    __syncthreads();
+  };
+  for (int t = 0; t < n; t += 2) {
+    step(t, tile0, tile1);
+    if (t + 1 >= n) break;
+    step(t + 1, tile1, tile0);
   }
 
   // ---- epilogue
-  const float l_tot = pair_sum(l_run);
-  if (!row_valid) return;
-  if (a.nsplit == 1) {
-    const float inv = 1.0f / l_tot;
-    T* op = reinterpret_cast<T*>(a.out) + qrow * D;
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
+  for (int b = 0; b < NB; ++b) {
+    const float l_tot = pair_sum(l_run[b]);
+    if (!row_valid[b]) continue;
+    if (a.nsplit == 1) {
+      const float inv = 1.0f / l_tot;
+      T* op = reinterpret_cast<T*>(a.out) + qrow[b] * D;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int d = dt * 32 + 8 * i + 4 * hh;
-        store4(op + d, o[dt][4 * i] * inv, o[dt][4 * i + 1] * inv, o[dt][4 * i + 2] * inv, o[dt][4 * i + 3] * inv);
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int d = dt * 32 + 8 * i + 4 * hh;
+          store4(op + d, o[b][dt][4 * i] * inv, o[b][dt][4 * i + 1] * inv, o[b][dt][4 * i + 2] * inv,
+                 o[b][dt][4 * i + 3] * inv);
+        }
+      if (a.lse != nullptr && hh == 0) a.lse[qrow[b]] = (m_ref[b] + __builtin_log2f(l_tot)) * kLn2;
+    } else {
+      const int64_t prow = (int64_t)split * a.total_rows * a.num_q_heads + qrow[b];
+      float* op = a.part_o + prow * D;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int d = dt * 32 + 8 * i + 4 * hh;
+          store4(op + d, o[b][dt][4 * i], o[b][dt][4 * i + 1], o[b][dt][4 * i + 2], o[b][dt][4 * i + 3]);
+        }
+      if (hh == 0) {
+        a.part_ml[prow * 2] = m_ref[b];
+        a.part_ml[prow * 2 + 1] = l_tot;
       }
-    if (a.lse != nullptr && hh == 0) a.lse[qrow] = (m_ref + __builtin_log2f(l_tot)) * kLn2;
-  } else {
-    const int64_t prow = (int64_t)split * a.total_rows * a.num_q_heads + qrow;
-    float* op = a.part_o + prow * D;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int d = dt * 32 + 8 * i + 4 * hh;
-        store4(op + d, o[dt][4 * i], o[dt][4 * i + 1], o[dt][4 * i + 2], o[dt][4 * i + 3]);
-      }
-    if (hh == 0) {
-      a.part_ml[prow * 2] = m_ref;
-      a.part_ml[prow * 2 + 1] = l_tot;
     }
   }
 }

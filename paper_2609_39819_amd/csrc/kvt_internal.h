@@ -15,7 +15,7 @@ constexpr int kSeqsPerLaunch = 64;  // sequences described by one launch
 
 // Extend tiling: one workgroup = 8 waves x 32 packed query rows, 64-key tiles.
 constexpr int kExtWaves = 8;
-constexpr int kExtRowsPerWave = 32;
+constexpr int kExtRowsPerWave = 32;    // one 32-row MFMA block
 constexpr int kExtTileRows = kExtWaves * kExtRowsPerWave;   // 256
 constexpr int kExtKeysPerTile = 64;
 constexpr int kMaxSplits = 16;
