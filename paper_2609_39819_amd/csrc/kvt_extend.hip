@@ -325,7 +325,9 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
         for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[b][half][e]);
       const float mxc = pair_max(mx) * c;
       const float m_new = (mxc > m_ref[b] + kRescaleSlack) ? mxc : m_ref[b];
-      alpha[b] = __builtin_amdgcn_exp2f(m_ref[b] - m_new);   // 1 when unchanged, 0 from -inf
+      // 1 when unchanged, 0 when leaving -inf; kept at 1 while the row has
+      // seen no visible key (a key split can lie wholly past a row's limit)
+      alpha[b] = (m_new == -INFINITY) ? 1.0f : __builtin_amdgcn_exp2f(m_ref[b] - m_new);
       m_ref[b] = m_new;
       l_run[b] *= alpha[b];
       moved = moved || alpha[b] != 1.0f;

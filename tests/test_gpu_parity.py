@@ -172,6 +172,8 @@ EDGE = [
     ([1000, 0, 47], [70, 300, 1], 12, 1, 128, "bf16"),
     ([63, 64, 65], [64, 65, 63], 16, 8, 64, "bf16"),
     ([2047], [129], 2, 2, 128, "bf16"),
+    # 15 key splits; rows 256..306 see no visible key in the last split
+    ([15821], [1000], 1, 1, 128, "bf16"),
 ]
 
 
