@@ -78,6 +78,29 @@ def cpu_baseline(w, target_s: float):
     }
 
 
+def sample_power(step, ms_per_step: float):
+    """Socket power and GFX clocks while steps run back to back: about 4 s of
+    steps are queued, amd-smi is read 1.5 s in, then the queue drains."""
+    import re
+    import subprocess
+    import torch
+    n = max(10, int(4000.0 / max(ms_per_step, 1e-3)))
+    for _ in range(n):
+        step()
+    time.sleep(1.5)
+    try:
+        r = subprocess.run(["amd-smi", "metric", "-p", "-c"], capture_output=True, text=True, timeout=60)
+        text = r.stdout
+    except (OSError, subprocess.TimeoutExpired) as e:
+        text = ""
+        log(f"amd-smi unavailable: {e}")
+    torch.cuda.synchronize()
+    power = re.search(r"SOCKET_POWER:\s*([0-9.]+)\s*W", text)
+    clocks = [int(x) for x in re.findall(r"GFX_\d+:\s*\n\s*CLK:\s*([0-9]+)\s*MHz", text)]
+    return {"socket_power_w": float(power.group(1)) if power else None,
+            "gfx_clock_mhz": clocks or None, "source": "amd-smi metric -p -c"}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -86,6 +109,9 @@ def main():
     ap.add_argument("--workload", default="react_128k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--sample-power", action="store_true",
+                    help="after the timed steps, keep the extend kernel running for a few seconds and "
+                         "record socket power and GFX clocks from amd-smi (reported, not timed)")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="run one plain fp32 copy kernel (torch.neg) of this size first, as the "
                          "reference a rocprofv3 FETCH_SIZE/WRITE_SIZE pass is scaled by")
@@ -194,6 +220,8 @@ def main():
         },
         "gpu": torch.cuda.get_device_name(dev),
     }
+    if args.sample_power:
+        res["power_sample"] = sample_power(lambda: step(), ms_per_step)
     del d, out, ws
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:

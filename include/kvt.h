@@ -37,8 +37,9 @@
  *   non-OK return nothing has been enqueued.  KVT_ERR_DEVICE reports a failed
  *   launch; kvt_last_hip_error() then returns the hipError_t (per thread).
  * Unchecked block ids: without a host mirror of the block table (checked
- *   mode off), an out-of-range id is never dereferenced: extend reads zeros
- *   for it and append skips it; the result is then unspecified, not a fault.
+ *   mode off), an out-of-range id is never dereferenced: extend clamps it to
+ *   the last page of the pool and append skips it; the result is then
+ *   unspecified, not a fault.
  */
 #ifndef KVT_H_
 #define KVT_H_
