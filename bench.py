@@ -70,8 +70,15 @@ def cpu_baseline(w, target_s: float):
         dt, fl, nt = run(n)
     tflops = fl / dt / 1e12
     toks = nt / dt
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), "")
+    except OSError:
+        pass
     return {
         "value": tflops, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+        "cpu_model": model, "nproc": os.cpu_count(),
         "sample": f"{nt} of {w.total_tokens} new tokens (evenly spaced), all {w.num_q_heads} query heads, "
                   f"full reused prefix; fp64 numpy oracle; {dt:.1f} s",
         "seconds": dt, "new_tokens_per_s": toks,
@@ -109,6 +116,9 @@ def main():
     ap.add_argument("--workload", default="react_128k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cold-mib", type=int, default=0,
+                    help="write a scratch buffer of this size before every step, outside the timed "
+                         "region, so the step starts with cold caches; times then come from HIP events")
     ap.add_argument("--sample-power", action="store_true",
                     help="after the timed steps, keep the extend kernel running for a few seconds and "
                          "record socket power and GFX clocks from amd-smi (reported, not timed)")
@@ -164,6 +174,7 @@ def main():
         torch.neg(calib_src, out=dst)
         torch.cuda.synchronize()
         del calib_src, dst
+    scratch = torch.empty(args.cold_mib * 262144, dtype=torch.float32, device=dev) if args.cold_mib else None
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -171,12 +182,16 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
+        if scratch is not None:
+            scratch.fill_(float(i))
         step(evs[i])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     app_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
     ext_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
-    ms_per_step = wall * 1e3 / args.steps
+    # with cold caches the scratch writes sit between the steps, so the step
+    # time is the sum of the kernels' event times instead of the wall clock
+    ms_per_step = float((app_ms + ext_ms).mean()) if scratch is not None else wall * 1e3 / args.steps
     value = flops / (ms_per_step * 1e-3) / 1e12
     ext_avg = float(ext_ms.mean())
     achieved = flops / (ext_avg * 1e-3) / 1e12
@@ -207,6 +222,9 @@ def main():
         "new_tokens_per_s": w.total_tokens / (ms_per_step * 1e-3),
         "pct_bf16_peak": 100.0 * value / PEAK_BF16_TFLOPS,
         "extend_ms": ext_avg,
+        "extend_ms_median": float(np.median(ext_ms)),
+        "extend_ms_min": float(ext_ms.min()),
+        "caches": f"cold ({args.cold_mib} MiB scratch write before each step)" if args.cold_mib else "warm",
         "extend_tflops": achieved,
         "append_ms": float(app_ms.mean()),
         "append_gbps": append_bytes / (float(app_ms.mean()) * 1e-3) / 1e9,
@@ -219,10 +237,12 @@ def main():
             "traffic": load_traffic(w.name),
         },
         "gpu": torch.cuda.get_device_name(dev),
+        "gcn_arch": torch.cuda.get_device_properties(dev).gcnArchName,
+        "hip": torch.version.hip,
     }
     if args.sample_power:
         res["power_sample"] = sample_power(lambda: step(), ms_per_step)
-    del d, out, ws
+    del d, out, ws, scratch
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on a sample")

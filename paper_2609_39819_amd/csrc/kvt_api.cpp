@@ -120,14 +120,18 @@ ExtendPlan make_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t num_q_h
     min_keys = std::min<int64_t>(min_keys, (int64_t)seqs->prefix_len[b] + 1);
   }
   const int cus = device_cus();
+  // Split the key range when whole rounds of workgroups over the CUs leave
+  // many CUs idle: with ns splits a unit's work shrinks to 1/ns and the call
+  // takes about ceil(units*ns / cus) / ns unit-times.  Take the smallest ns
+  // with the best estimate if it beats no split by at least 10 %; each split
+  // keeps at least 16 key tiles (1024 keys) of the shortest sequence.
+  const int64_t by_keys = std::max<int64_t>(1, min_keys / (16 * kvt::kExtKeysPerTile));
+  const int ns_max = (int)std::min<int64_t>(by_keys, kvt::kMaxSplits);
+  auto rounds = [&](int s) { return (double)((units * s + cus - 1) / cus) / s; };
   int ns = 1;
-  if (units < cus) {
-    ns = (int)((cus + units - 1) / units);
-    // each split keeps at least 16 key tiles (1024 keys) of the shortest sequence
-    const int64_t by_keys = std::max<int64_t>(1, min_keys / (16 * kvt::kExtKeysPerTile));
-    ns = (int)std::min<int64_t>({(int64_t)ns, by_keys, (int64_t)kvt::kMaxSplits});
-    ns = std::max(ns, 1);
-  }
+  for (int s = 2; s <= ns_max; ++s)
+    if (rounds(s) < rounds(ns) - 1e-9) ns = s;
+  if (rounds(ns) > 0.9 * rounds(1)) ns = 1;
   p.nsplit = ns;
   if (ns > 1) {
     const int64_t rows = T * num_q_heads;

@@ -288,6 +288,9 @@ def build_workload(
 # --------------------------------------------------------------------------
 
 CONFIG_NAMES = ("tiny", "gqa_8k", "react_128k", "forked_agents", "mutation_258k")
+# one GPU's share of the 128K turn under 4-way tensor parallelism (heads split
+# with no communication: 24 query heads over 2 kv-heads per GPU)
+EXTRA_CONFIG_NAMES = ("react_128k_tp4",)
 
 
 def config_shapes(name: str) -> dict:
@@ -300,6 +303,9 @@ def config_shapes(name: str) -> dict:
                     num_blocks=65536, prefix=8192, suffix=512)
     if name == "react_128k":
         return dict(seed=3, num_q_heads=96, num_kv_heads=8, head_dim=128, dtype="bf16",
+                    num_blocks=1 << 20, prefix=131072, suffix=2048)
+    if name == "react_128k_tp4":
+        return dict(seed=6, num_q_heads=24, num_kv_heads=2, head_dim=128, dtype="bf16",
                     num_blocks=1 << 20, prefix=131072, suffix=2048)
     if name == "forked_agents":
         return dict(seed=4, num_q_heads=96, num_kv_heads=8, head_dim=128, dtype="bf16",

@@ -19,8 +19,10 @@ from gpu_common import (cached_config, compare, gather_rows, oracle_pools, run_a
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
-SAMPLE = {"tiny": None, "gqa_8k": None, "react_128k": 48, "forked_agents": 6, "mutation_258k": 16}
-ALL = ["tiny", "gqa_8k", "react_128k", "forked_agents", "mutation_258k"]
+SAMPLE = {"tiny": None, "gqa_8k": None, "react_128k": 48, "forked_agents": 6, "mutation_258k": 16,
+          "react_128k_tp4": 48}
+# the five workloads, plus one GPU's share of the 128K turn under 4-way head parallelism
+ALL = ["tiny", "gqa_8k", "react_128k", "forked_agents", "mutation_258k", "react_128k_tp4"]
 
 
 @pytest.fixture(scope="module", autouse=True)

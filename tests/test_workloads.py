@@ -73,3 +73,16 @@ def test_flop_and_byte_counters_match_hand_values():
 
 def test_block_size_is_sixteen():
     assert BLOCK_SIZE == 16
+
+
+def test_tp4_shard_shape():
+    """One GPU's share of the 128K turn under 4-way head parallelism: a quarter
+    of the heads and of the work, same lengths."""
+    from paper_2609_39819_amd.workloads import algorithmic_flops, config_shapes
+    c, full = config_shapes("react_128k_tp4"), config_shapes("react_128k")
+    assert (c["num_q_heads"], c["num_kv_heads"]) == (full["num_q_heads"] // 4, full["num_kv_heads"] // 4)
+    assert (c["prefix"], c["suffix"]) == (full["prefix"], full["suffix"])
+    f4 = algorithmic_flops([c["prefix"]], [c["suffix"]], c["num_q_heads"], c["head_dim"])
+    f1 = algorithmic_flops([full["prefix"]], [full["suffix"]], full["num_q_heads"], full["head_dim"])
+    # 4*D*Hq*(S*P + S(S+1)/2) = 4*128*96*(2048*131072 + 2048*2049/2)
+    assert 4 * f4 == f1 == 49152 * 270533632
