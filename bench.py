@@ -24,6 +24,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "extend-attention TFLOP/s and new tokens/s at 128K reused prefix; % bf16 MFMA peak"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X published dense bf16 MFMA peak
+PEAK_HBM_GBPS = 8000.0      # MI355X published HBM3E bandwidth
 
 
 def log(*a):
@@ -132,7 +133,7 @@ def main():
 
     import torch
     from paper_2609_39819_amd import kvt
-    from paper_2609_39819_amd.workloads import algorithmic_flops, make_config, stage_on_device
+    from paper_2609_39819_amd.workloads import algorithmic_flops, kv_bytes, make_config, stage_on_device
 
     kvt.lib()   # fail loudly if the library is missing
     dev = torch.device("cuda", 0)
@@ -152,8 +153,15 @@ def main():
     flops = algorithmic_flops(w.prefix_len, w.suffix_len, Hq, D)
     elem = 2 if w.dtype == "bf16" else 4
     append_bytes = 2 * 2 * w.total_tokens * w.num_kv_heads * D * elem   # K+V, read + write
+    # a decoding step (one new token per sequence) runs the decode kernel,
+    # which is bound by streaming K/V from HBM
+    decode = w.name.startswith("decode")
+    attn_bytes = kv_bytes(w.prefix_len, w.suffix_len, w.num_kv_heads, D, elem) + 2 * w.total_tokens * Hq * D * elem
     out = torch.empty_like(d["q"])
-    need = kvt.extend_workspace_bytes(d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.suffix_len, Hq)
+    if decode:
+        need = kvt.decode_workspace_bytes(d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, Hq)
+    else:
+        need = kvt.extend_workspace_bytes(d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.suffix_len, Hq)
     ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev) if need else None
     stream = torch.cuda.current_stream(dev)
 
@@ -163,8 +171,12 @@ def main():
         kvt.append_kv(d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.suffix_len, d["k_new"], d["v_new"])
         if ev is not None:
             ev[1].record(stream)
-        kvt.extend_attention(d["q"], d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.suffix_len,
-                             w.scale, out=out, workspace=ws, use_workspace=need > 0)
+        if decode:
+            kvt.decode_attention(d["q"], d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.scale,
+                                 out=out, workspace=ws, use_workspace=need > 0)
+        else:
+            kvt.extend_attention(d["q"], d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.suffix_len,
+                                 w.scale, out=out, workspace=ws, use_workspace=need > 0)
         if ev is not None:
             ev[2].record(stream)
 
@@ -221,6 +233,7 @@ def main():
         },
         "new_tokens_per_s": w.total_tokens / (ms_per_step * 1e-3),
         "pct_bf16_peak": 100.0 * value / PEAK_BF16_TFLOPS,
+        "attention_kernel": "decode" if decode else "extend",
         "extend_ms": ext_avg,
         "extend_ms_median": float(np.median(ext_ms)),
         "extend_ms_min": float(ext_ms.min()),
@@ -235,6 +248,13 @@ def main():
             "unit": "TFLOP/s",
             "frac": achieved / PEAK_BF16_TFLOPS,
             "traffic": load_traffic(w.name),
+        } if not decode else {
+            "bound": "hbm",
+            "achieved": attn_bytes / (ext_avg * 1e-3) / 1e9,
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": attn_bytes / (ext_avg * 1e-3) / 1e9 / PEAK_HBM_GBPS,
+            "traffic": None,
         },
         "gpu": torch.cuda.get_device_name(dev),
         "gcn_arch": torch.cuda.get_device_properties(dev).gcnArchName,

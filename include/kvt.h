@@ -128,6 +128,36 @@ kvt_status kvt_extend_attention(const kvt_pool* pool, const kvt_seqs* seqs,
  * the arguments are invalid.  Host-only; enqueues nothing. */
 size_t kvt_extend_workspace_bytes(const kvt_pool* pool, const kvt_seqs* seqs, int32_t num_q_heads);
 
+/*
+ * kvt_decode_attention -- one decoding step: attention of each sequence's
+ * single new token over its whole cache (paper section 5.2: once a request's
+ * prefill completes, LLM decoding proceeds token by token over the same KV).
+ *
+ * The same operation as kvt_extend_attention with S_b = 1 for every b (the
+ * new token at position P_b sees keys 0..P_b, its own K/V appended first by
+ * kvt_append_kv):
+ *   out[b][h] = sum_j softmax(scale * <q[b][h], K_b[j]>)_j V_b[j],  j = 0 .. P_b
+ *   lse[b][h] = ln sum_j exp(scale * <q[b][h], K_b[j]>)            (optional)
+ * Row b of q/out/lse is sequence b.  Built for large batches whose cost is
+ * streaming every sequence's K/V once from HBM.
+ *
+ * Arguments as for kvt_extend_attention, and: every suffix_len[b] must be 1
+ * (else KVT_ERR_INVALID_ARG); Hq/Hkv must be at most 32 (else
+ * KVT_ERR_UNSUPPORTED).  workspace: device scratch for key-split partial
+ * results; NULL/0 runs unsplit, otherwise at least
+ * kvt_decode_workspace_bytes() for the same arguments (else
+ * KVT_ERR_WORKSPACE).  Results are bit-reproducible for given arguments.
+ */
+kvt_status kvt_decode_attention(const kvt_pool* pool, const kvt_seqs* seqs,
+                                const void* q, int32_t num_q_heads, float scale,
+                                void* out, float* lse,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace that lets kvt_decode_attention split each sequence's keys over
+ * several workgroups (small batches).  0 when no split is planned or the
+ * arguments are invalid.  Host-only; enqueues nothing. */
+size_t kvt_decode_workspace_bytes(const kvt_pool* pool, const kvt_seqs* seqs, int32_t num_q_heads);
+
 /* Static English text for a status code (never NULL). */
 const char* kvt_status_str(kvt_status s);
 

@@ -142,6 +142,87 @@ ExtendPlan make_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t num_q_h
   return p;
 }
 
+// Decode: one unit per (sequence, key split) and kv-head.  Splits are added
+// while the workgroups cannot cover the CUs twice over, keeping at least 1024
+// keys of the shortest sequence per split (each of the 4 waves then streams
+// at least 8 tiles of 32 keys).
+ExtendPlan make_decode_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t num_q_heads) {
+  ExtendPlan p;
+  const int B = seqs->num_seqs;
+  p.order.resize(B);
+  std::iota(p.order.begin(), p.order.end(), 0);
+  std::stable_sort(p.order.begin(), p.order.end(),
+                   [&](int x, int y) { return seqs->prefix_len[x] > seqs->prefix_len[y]; });
+  int64_t min_keys = INT64_MAX;
+  for (int b = 0; b < B; ++b) min_keys = std::min<int64_t>(min_keys, (int64_t)seqs->prefix_len[b] + 1);
+  const int64_t units = (int64_t)B * pool->num_kv_heads;
+  const int64_t want = (2 * (int64_t)device_cus() + units - 1) / units;
+  const int64_t by_keys = std::max<int64_t>(1, min_keys / 1024);
+  p.nsplit = (int)std::max<int64_t>(1, std::min<int64_t>({want, by_keys, (int64_t)kvt::kMaxSplits}));
+  if (p.nsplit > 1) {
+    const int64_t rows = (int64_t)B * num_q_heads;
+    const size_t o_bytes = (size_t)p.nsplit * rows * pool->head_dim * sizeof(float);
+    const size_t ml_bytes = (size_t)p.nsplit * rows * 2 * sizeof(float);
+    p.ws_bytes = ((o_bytes + 255) / 256) * 256 + ml_bytes;
+  }
+  return p;
+}
+
+// out must not overlap q or a pool; lse must not overlap out.
+kvt_status check_outputs(const kvt_pool* pool, const void* q, int32_t num_q_heads, const void* out,
+                         const float* lse, int64_t T) {
+  const size_t es = elem_bytes(pool->dtype);
+  const size_t tok_bytes = (size_t)T * num_q_heads * pool->head_dim * es;
+  const size_t pool_bytes = (size_t)pool->num_blocks * pool->num_kv_heads * kvt::kBlock * pool->head_dim * es;
+  if (overlaps(out, tok_bytes, q, tok_bytes) || overlaps(out, tok_bytes, pool->k, pool_bytes) ||
+      overlaps(out, tok_bytes, pool->v, pool_bytes))
+    return KVT_ERR_INVALID_ARG;
+  if (lse != nullptr && overlaps(lse, (size_t)T * num_q_heads * sizeof(float), out, tok_bytes))
+    return KVT_ERR_INVALID_ARG;
+  return KVT_OK;
+}
+
+// Launch arguments common to extend and decode.
+kvt::ExtendArgs base_args(const kvt_pool* pool, const kvt_seqs* seqs, const void* q, int32_t num_q_heads,
+                          float scale, void* out, float* lse, int64_t T, const ExtendPlan& plan, void* workspace) {
+  kvt::ExtendArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.q = q;
+  a.k_pool = pool->k;
+  a.v_pool = pool->v;
+  a.out = out;
+  a.lse = lse;
+  a.block_table = seqs->block_table;
+  a.num_blocks = pool->num_blocks;
+  a.max_blocks = seqs->max_blocks;
+  a.num_q_heads = num_q_heads;
+  a.num_kv_heads = pool->num_kv_heads;
+  a.group = num_q_heads / pool->num_kv_heads;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.nsplit = plan.nsplit;
+  a.total_rows = (int32_t)T;
+  if (plan.nsplit > 1) {
+    const size_t o_bytes = (size_t)plan.nsplit * T * num_q_heads * pool->head_dim * sizeof(float);
+    a.part_o = reinterpret_cast<float*>(workspace);
+    a.part_ml = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + ((o_bytes + 255) / 256) * 256);
+  }
+  return a;
+}
+
+// Merge of the per-split partial results into out (and lse).
+kvt_status combine(const kvt::ExtendArgs& a, const kvt_pool* pool, void* out, float* lse, int64_t T,
+                   int32_t num_q_heads, int nsplit, hipStream_t s) {
+  kvt::CombineArgs c;
+  c.part_o = a.part_o;
+  c.part_ml = a.part_ml;
+  c.out = out;
+  c.lse = lse;
+  c.rows = T * num_q_heads;
+  c.nsplit = nsplit;
+  const hipError_t e = kvt::launch_combine(c, pool->dtype, pool->head_dim, s);
+  return e == hipSuccess ? KVT_OK : device_error(e);
+}
+
 }  // namespace
 
 extern "C" {
@@ -235,14 +316,7 @@ kvt_status kvt_extend_attention(const kvt_pool* pool, const kvt_seqs* seqs, cons
   if (num_q_heads < 1 || num_q_heads % pool->num_kv_heads != 0) return KVT_ERR_INVALID_ARG;
   if (!(scale > 0.f) || !std::isfinite(scale)) return KVT_ERR_INVALID_ARG;
   if ((st = check_table_ids(pool, seqs)) != KVT_OK) return st;
-  const size_t es = elem_bytes(pool->dtype);
-  const size_t tok_bytes = (size_t)T * num_q_heads * pool->head_dim * es;
-  const size_t pool_bytes = (size_t)pool->num_blocks * pool->num_kv_heads * kvt::kBlock * pool->head_dim * es;
-  if (overlaps(out, tok_bytes, q, tok_bytes) || overlaps(out, tok_bytes, pool->k, pool_bytes) ||
-      overlaps(out, tok_bytes, pool->v, pool_bytes))
-    return KVT_ERR_INVALID_ARG;
-  if (lse != nullptr && overlaps(lse, (size_t)T * num_q_heads * sizeof(float), out, tok_bytes))
-    return KVT_ERR_INVALID_ARG;
+  if ((st = check_outputs(pool, q, num_q_heads, out, lse, T)) != KVT_OK) return st;
 
   ExtendPlan plan = make_plan(pool, seqs, num_q_heads, T);
   if (plan.nsplit > 1) {
@@ -258,27 +332,7 @@ kvt_status kvt_extend_attention(const kvt_pool* pool, const kvt_seqs* seqs, cons
   std::vector<int32_t> row_off(seqs->num_seqs + 1, 0);
   for (int b = 0; b < seqs->num_seqs; ++b) row_off[b + 1] = row_off[b] + seqs->suffix_len[b];
 
-  kvt::ExtendArgs a;
-  std::memset(&a, 0, sizeof(a));
-  a.q = q;
-  a.k_pool = pool->k;
-  a.v_pool = pool->v;
-  a.out = out;
-  a.lse = lse;
-  a.block_table = seqs->block_table;
-  a.num_blocks = pool->num_blocks;
-  a.max_blocks = seqs->max_blocks;
-  a.num_q_heads = num_q_heads;
-  a.num_kv_heads = pool->num_kv_heads;
-  a.group = G;
-  a.scale_log2 = scale * 1.4426950408889634f;
-  a.nsplit = plan.nsplit;
-  a.total_rows = (int32_t)T;
-  if (plan.nsplit > 1) {
-    const size_t o_bytes = (size_t)plan.nsplit * T * num_q_heads * pool->head_dim * sizeof(float);
-    a.part_o = reinterpret_cast<float*>(workspace);
-    a.part_ml = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + ((o_bytes + 255) / 256) * 256);
-  }
+  kvt::ExtendArgs a = base_args(pool, seqs, q, num_q_heads, scale, out, lse, T, plan, workspace);
   for (size_t c0 = 0; c0 < plan.order.size(); c0 += kvt::kSeqsPerLaunch) {
     const int n = (int)std::min<size_t>(kvt::kSeqsPerLaunch, plan.order.size() - c0);
     a.nseq = n;
@@ -295,18 +349,57 @@ kvt_status kvt_extend_attention(const kvt_pool* pool, const kvt_seqs* seqs, cons
     const hipError_t e = kvt::launch_extend(a, pool->dtype, pool->head_dim, (int)grid, s);
     if (e != hipSuccess) return device_error(e);
   }
+  return plan.nsplit > 1 ? combine(a, pool, out, lse, T, num_q_heads, plan.nsplit, s) : KVT_OK;
+}
+
+size_t kvt_decode_workspace_bytes(const kvt_pool* pool, const kvt_seqs* seqs, int32_t num_q_heads) {
+  if (check_pool(pool) != KVT_OK) return 0;
+  int64_t T = 0;
+  if (check_seqs(seqs, &T) != KVT_OK || T != seqs->num_seqs) return 0;
+  if (num_q_heads < 1 || num_q_heads % pool->num_kv_heads != 0) return 0;
+  if (num_q_heads / pool->num_kv_heads > kvt::kDecMaxGroup) return 0;
+  return make_decode_plan(pool, seqs, num_q_heads).ws_bytes;
+}
+
+kvt_status kvt_decode_attention(const kvt_pool* pool, const kvt_seqs* seqs, const void* q, int32_t num_q_heads,
+                                float scale, void* out, float* lse, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  kvt_status st = check_pool(pool);
+  if (st != KVT_OK) return st;
+  int64_t T = 0;
+  if ((st = check_seqs(seqs, &T)) != KVT_OK) return st;
+  if (T != seqs->num_seqs) return KVT_ERR_INVALID_ARG;   // one new token per sequence
+  if (q == nullptr || out == nullptr) return KVT_ERR_INVALID_ARG;
+  if (num_q_heads < 1 || num_q_heads % pool->num_kv_heads != 0) return KVT_ERR_INVALID_ARG;
+  if (num_q_heads / pool->num_kv_heads > kvt::kDecMaxGroup) return KVT_ERR_UNSUPPORTED;
+  if (!(scale > 0.f) || !std::isfinite(scale)) return KVT_ERR_INVALID_ARG;
+  if ((st = check_table_ids(pool, seqs)) != KVT_OK) return st;
+  if ((st = check_outputs(pool, q, num_q_heads, out, lse, T)) != KVT_OK) return st;
+
+  ExtendPlan plan = make_decode_plan(pool, seqs, num_q_heads);
   if (plan.nsplit > 1) {
-    kvt::CombineArgs c;
-    c.part_o = a.part_o;
-    c.part_ml = a.part_ml;
-    c.out = out;
-    c.lse = lse;
-    c.rows = T * num_q_heads;
-    c.nsplit = plan.nsplit;
-    const hipError_t e = kvt::launch_combine(c, pool->dtype, pool->head_dim, s);
+    if (workspace == nullptr && workspace_bytes == 0) {
+      plan.nsplit = 1;
+    } else if (workspace == nullptr || workspace_bytes < plan.ws_bytes) {
+      return KVT_ERR_WORKSPACE;
+    }
+  }
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  kvt::ExtendArgs a = base_args(pool, seqs, q, num_q_heads, scale, out, lse, T, plan, workspace);
+  for (size_t c0 = 0; c0 < plan.order.size(); c0 += kvt::kSeqsPerLaunch) {
+    const int n = (int)std::min<size_t>(kvt::kSeqsPerLaunch, plan.order.size() - c0);
+    a.nseq = n;
+    for (int i = 0; i < n; ++i) {
+      const int b = plan.order[c0 + i];
+      a.seq[i] = kvt::SeqDesc{b, seqs->prefix_len[b], 1, b};   // row of sequence b is b
+      a.unit_begin[i] = i * plan.nsplit;
+    }
+    a.unit_begin[n] = n * plan.nsplit;
+    const int64_t grid = (int64_t)n * plan.nsplit * pool->num_kv_heads;
+    const hipError_t e = kvt::launch_decode(a, pool->dtype, pool->head_dim, (int)grid, s);
     if (e != hipSuccess) return device_error(e);
   }
-  return KVT_OK;
+  return plan.nsplit > 1 ? combine(a, pool, out, lse, T, num_q_heads, plan.nsplit, s) : KVT_OK;
 }
 
 }  // extern "C"

@@ -20,6 +20,12 @@ constexpr int kExtTileRows = kExtWaves * kExtRowsPerWave;   // 256
 constexpr int kExtKeysPerTile = 64;
 constexpr int kMaxSplits = 16;
 
+// Decode tiling: one workgroup = 4 waves over one (sequence, kv-head, key
+// split); each wave streams its own 32-key tiles; up to 32 query rows (G).
+constexpr int kDecWaves = 4;
+constexpr int kDecKeysPerTile = 32;
+constexpr int kDecMaxGroup = 32;
+
 struct SeqDesc {
   int32_t seq;      // row of the block table
   int32_t prefix;   // P_b
@@ -77,5 +83,7 @@ struct CombineArgs {
 hipError_t launch_append(const AppendArgs& a, int dtype, int head_dim, hipStream_t stream);
 hipError_t launch_extend(const ExtendArgs& a, int dtype, int head_dim, int grid, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, int dtype, int head_dim, hipStream_t stream);
+// Decode: ExtendArgs with suffix 1 per sequence and nsplit units per sequence.
+hipError_t launch_decode(const ExtendArgs& a, int dtype, int head_dim, int grid, hipStream_t stream);
 
 }  // namespace kvt

@@ -27,8 +27,8 @@ KVT_DTYPE_BF16 = 0
 KVT_DTYPE_F32 = 1
 BLOCK_SIZE = 16
 
-EXPORTED = ("kvt_append_kv", "kvt_extend_attention", "kvt_extend_workspace_bytes",
-            "kvt_status_str", "kvt_last_hip_error")
+EXPORTED = ("kvt_append_kv", "kvt_decode_attention", "kvt_decode_workspace_bytes", "kvt_extend_attention",
+            "kvt_extend_workspace_bytes", "kvt_last_hip_error", "kvt_status_str")
 
 
 class KvtPool(ctypes.Structure):
@@ -68,6 +68,10 @@ def lib():
         L.kvt_extend_attention.restype = ctypes.c_int
         L.kvt_extend_workspace_bytes.argtypes = [P(KvtPool), P(KvtSeqs), ctypes.c_int32]
         L.kvt_extend_workspace_bytes.restype = ctypes.c_size_t
+        L.kvt_decode_attention.argtypes = L.kvt_extend_attention.argtypes
+        L.kvt_decode_attention.restype = ctypes.c_int
+        L.kvt_decode_workspace_bytes.argtypes = L.kvt_extend_workspace_bytes.argtypes
+        L.kvt_decode_workspace_bytes.restype = ctypes.c_size_t
         L.kvt_status_str.argtypes = [ctypes.c_int]
         L.kvt_status_str.restype = ctypes.c_char_p
         L.kvt_last_hip_error.argtypes = []
@@ -177,6 +181,29 @@ def extend_attention(q, k_pool, v_pool, block_table, prefix_len: Sequence[int], 
     of at least ``extend_workspace_bytes`` (allocated here when
     ``use_workspace`` and none is given).
     """
+    return _attention("kvt_extend_attention", "kvt_extend_workspace_bytes", q, k_pool, v_pool, block_table,
+                      prefix_len, suffix_len, scale, out, lse, return_lse, workspace, use_workspace, stream, checked)
+
+
+def decode_workspace_bytes(k_pool, v_pool, block_table, prefix_len, num_q_heads: int) -> int:
+    pool = _pool_struct(k_pool, v_pool)
+    seqs = _seqs(prefix_len, np.ones(len(prefix_len), dtype=np.int32), block_table, False)
+    return int(lib().kvt_decode_workspace_bytes(ctypes.byref(pool), ctypes.byref(seqs.struct), int(num_q_heads)))
+
+
+def decode_attention(q, k_pool, v_pool, block_table, prefix_len: Sequence[int], scale: Optional[float] = None, *,
+                     out=None, lse=None, return_lse: bool = False, workspace=None, use_workspace: bool = True,
+                     stream=None, checked: bool = False):
+    """One decoding step (``kvt_decode_attention``): row b of ``q`` ([B][Hq][D])
+    is the new token of sequence b at position ``prefix_len[b]``, whose K/V
+    was appended first.  Returns ``out`` ([B][Hq][D]) or ``(out, lse)``."""
+    ones = np.ones(len(prefix_len), dtype=np.int32)
+    return _attention("kvt_decode_attention", "kvt_decode_workspace_bytes", q, k_pool, v_pool, block_table,
+                      prefix_len, ones, scale, out, lse, return_lse, workspace, use_workspace, stream, checked)
+
+
+def _attention(entry: str, ws_entry: str, q, k_pool, v_pool, block_table, prefix_len, suffix_len, scale, out, lse,
+               return_lse, workspace, use_workspace, stream, checked):
     import torch
     pool = _pool_struct(k_pool, v_pool)
     seqs = _seqs(prefix_len, suffix_len, block_table, checked)
@@ -198,13 +225,13 @@ def extend_attention(q, k_pool, v_pool, block_table, prefix_len: Sequence[int], 
     if workspace is not None:
         ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
     elif use_workspace:
-        need = int(lib().kvt_extend_workspace_bytes(ctypes.byref(pool), ctypes.byref(seqs.struct), Hq))
+        need = int(getattr(lib(), ws_entry)(ctypes.byref(pool), ctypes.byref(seqs.struct), Hq))
         if need:
             workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
             ws_ptr, ws_bytes = workspace.data_ptr(), need
-    st = lib().kvt_extend_attention(ctypes.byref(pool), ctypes.byref(seqs.struct), q.data_ptr(), Hq, float(scale),
-                                    out.data_ptr(), lse.data_ptr() if lse is not None else None, ws_ptr, ws_bytes,
-                                    _stream_handle(q.device, stream))
+    st = getattr(lib(), entry)(ctypes.byref(pool), ctypes.byref(seqs.struct), q.data_ptr(), Hq, float(scale),
+                               out.data_ptr(), lse.data_ptr() if lse is not None else None, ws_ptr, ws_bytes,
+                               _stream_handle(q.device, stream))
     if st != KVT_OK:
-        raise KvtError(st, "kvt_extend_attention")
+        raise KvtError(st, entry)
     return (out, lse) if want_lse else out

@@ -28,7 +28,8 @@ import os
 from typing import Dict, List
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-EXTEND_SOURCES = ("paper_2609_39819_amd/csrc/kvt_extend.hip", "paper_2609_39819_amd/csrc/kvt_internal.h")
+EXTEND_SOURCES = ("paper_2609_39819_amd/csrc/kvt_extend.hip", "paper_2609_39819_amd/csrc/kvt_device.h",
+                  "paper_2609_39819_amd/csrc/kvt_internal.h")
 EXTEND_KERNEL = "extend_fwd_kernel"
 COPY_KERNEL = "neg_kernel"
 

@@ -71,6 +71,13 @@ def _extend(pool, seqs, hq=4, scale=0.125, q=FAKE_Q, out=FAKE_OUT, ws=None, ws_b
                                   q, hq, scale, out, None, ws, ws_bytes, None)
 
 
+def _decode(pool, seqs, hq=4, scale=0.125, q=FAKE_Q, out=FAKE_OUT, ws=None, ws_bytes=0):
+    L = kvt.lib()
+    return L.kvt_decode_attention(ctypes.byref(pool) if pool is not None else None,
+                                  ctypes.byref(seqs.struct) if seqs is not None else None,
+                                  q, hq, scale, out, None, ws, ws_bytes, None)
+
+
 def _append(pool, seqs, kn=FAKE_Q, vn=FAKE_OUT):
     L = kvt.lib()
     return L.kvt_append_kv(ctypes.byref(pool) if pool is not None else None,
@@ -119,6 +126,41 @@ def test_extend_specific_checks():
     assert _extend(_pool(), _seqs(), scale=float("inf")) == E
     assert _extend(_pool(), _seqs(), out=FAKE_Q + 64) == E           # out overlaps q
     assert _extend(_pool(), _seqs(), out=FAKE_K + 128) == E          # out inside the K pool
+
+
+@no_gpu_only
+def test_decode_specific_checks():
+    E, U = kvt.KVT_ERR_INVALID_ARG, kvt.KVT_ERR_UNSUPPORTED
+    one = _seqs(S=(1,))
+    assert _decode(None, one) == E
+    assert _decode(_pool(), _seqs()) == E                            # suffix 16: not a decode step
+    assert _decode(_pool(), _seqs(P=(240, 240), S=(1, 2), max_blocks=16)) == E
+    assert _decode(_pool(), one, q=0) == E
+    assert _decode(_pool(), one, out=0) == E
+    assert _decode(_pool(hkv=2), one, hq=3) == E
+    assert _decode(_pool(), one, scale=0.0) == E
+    assert _decode(_pool(), one, out=FAKE_Q + 64) == E
+    assert _decode(_pool(), one, hq=33) == U                         # more than 32 query heads per kv-head
+    assert _decode(_pool(d=96), one) == U
+    host = np.arange(16, dtype=np.int32).reshape(1, 16); host[0, 3] = 64
+    assert _decode(_pool(), _seqs(S=(1,), host=host)) == kvt.KVT_ERR_OUT_OF_RANGE
+
+
+def test_decode_workspace_bytes_follow_the_split_plan():
+    def ws(pool, seqs, hq):
+        return kvt.lib().kvt_decode_workspace_bytes(ctypes.byref(pool), ctypes.byref(seqs.struct), hq)
+    pool = _pool(nb=1 << 20, hkv=8, d=128)
+    # 4 sequences x 8 kv-heads = 32 units: splits until 512 workgroups, capped at 16
+    s = _seqs(P=(65535, 40000, 30000, 20000), S=(1, 1, 1, 1), max_blocks=4096)
+    rows = 4 * 96
+    assert ws(pool, s, 96) == 16 * rows * 128 * 4 + 16 * rows * 2 * 4
+    # the shortest sequence keeps >= 1024 keys per split: 3000 keys -> 2 splits
+    s2 = _seqs(P=(65535, 2999), S=(1, 1), max_blocks=4096)
+    assert ws(pool, s2, 96) == 2 * 2 * 96 * 128 * 4 + 2 * 2 * 96 * 2 * 4
+    # 64 sequences x 8 kv-heads = 512 units: no split
+    s3 = _seqs(P=(4095,) * 64, S=(1,) * 64, max_blocks=256)
+    assert ws(pool, s3, 96) == 0
+    assert ws(pool, _seqs(), 96) == 0                                # not a decode step
 
 
 @no_gpu_only
