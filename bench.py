@@ -31,12 +31,13 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def load_traffic(workload: str):
-    """HBM bytes per extend launch from committed rocprofv3 counters, if they
-    were taken on the current kernel sources; else None."""
-    from paper_2609_39819_amd.profiling import read_traffic, source_sha
-    t = read_traffic(os.path.join(ROOT, "profiles", f"extend_{workload}_traffic.md"))
-    if t is None or t[0] != source_sha():
+def load_traffic(workload: str, decode: bool = False):
+    """HBM bytes per attention launch from committed rocprofv3 counters, if
+    they were taken on the current kernel sources; else None."""
+    from paper_2609_39819_amd.profiling import DECODE_SOURCES, EXTEND_SOURCES, read_traffic, source_sha
+    kind = "decode" if decode else "extend"
+    t = read_traffic(os.path.join(ROOT, "profiles", f"{kind}_{workload}_traffic.md"))
+    if t is None or t[0] != source_sha(DECODE_SOURCES if decode else EXTEND_SOURCES):
         return None
     return t[1]
 
@@ -254,7 +255,7 @@ def main():
             "peak": PEAK_HBM_GBPS,
             "unit": "GB/s",
             "frac": attn_bytes / (ext_avg * 1e-3) / 1e9 / PEAK_HBM_GBPS,
-            "traffic": None,
+            "traffic": load_traffic(w.name, decode=True),
         },
         "gpu": torch.cuda.get_device_name(dev),
         "gcn_arch": torch.cuda.get_device_properties(dev).gcnArchName,

@@ -30,8 +30,12 @@ from typing import Dict, List
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 EXTEND_SOURCES = ("paper_2609_39819_amd/csrc/kvt_extend.hip", "paper_2609_39819_amd/csrc/kvt_device.h",
                   "paper_2609_39819_amd/csrc/kvt_internal.h")
+DECODE_SOURCES = ("paper_2609_39819_amd/csrc/kvt_decode.hip", "paper_2609_39819_amd/csrc/kvt_device.h",
+                  "paper_2609_39819_amd/csrc/kvt_internal.h")
 EXTEND_KERNEL = "extend_fwd_kernel"
+DECODE_KERNEL = "decode_kernel"
 COPY_KERNEL = "neg_kernel"
+SOURCES = {EXTEND_KERNEL: EXTEND_SOURCES, DECODE_KERNEL: DECODE_SOURCES}
 
 
 def source_sha(paths=EXTEND_SOURCES) -> str:
@@ -46,7 +50,7 @@ def demangle(name: str) -> str:
     """Readable form of this library's kernel symbols (c++filt does not know
     the bf16 mangling DF16b)."""
     import re
-    m = re.search(r"(extend_fwd_kernel|extend_combine_kernel)I(DF16b|f)Li(\d+)E", name)
+    m = re.search(r"(extend_fwd_kernel|extend_combine_kernel|decode_kernel)I(DF16b|f)Li(\d+)E", name)
     if m:
         return f"{m.group(1)}<{'bf16' if m.group(2) == 'DF16b' else 'float'}, {m.group(3)}>"
     return name
@@ -54,7 +58,7 @@ def demangle(name: str) -> str:
 
 def short_name(name: str) -> str:
     name = demangle(name)
-    for key in ("extend_fwd_kernel", "extend_combine_kernel", "append_kv_kernel"):
+    for key in ("extend_fwd_kernel", "extend_combine_kernel", "decode_kernel", "append_kv_kernel"):
         if key in name:
             tmpl = name[name.find(key):]
             return tmpl.split("(")[0].replace("kvt::(anonymous namespace)::", "")
@@ -103,10 +107,11 @@ def cmd_traffic(args) -> str:
 
     fc = find(f, COPY_KERNEL)["FETCH_SIZE"] * 1024 / copy_bytes    # counter bytes per true byte
     wc = find(w, COPY_KERNEL)["WRITE_SIZE"] * 1024 / copy_bytes
-    fe = find(f, EXTEND_KERNEL)["FETCH_SIZE"] * 1024 / fc
-    we = find(w, EXTEND_KERNEL)["WRITE_SIZE"] * 1024 / wc
+    fe = find(f, args.kernel)["FETCH_SIZE"] * 1024 / fc
+    we = find(w, args.kernel)["WRITE_SIZE"] * 1024 / wc
+    what = "decode" if args.kernel == DECODE_KERNEL else "extend"
     lines = [
-        f"# HBM traffic per extend launch: {args.title}", "",
+        f"# HBM traffic per {what} launch: {args.title}", "",
         f"Command (FETCH_SIZE pass): `{args.cmd.replace('{C}', 'FETCH_SIZE')}`",
         f"Command (WRITE_SIZE pass): `{args.cmd.replace('{C}', 'WRITE_SIZE')}`", "",
         f"Calibration: a {args.copy_mib} MiB fp32 copy kernel (torch.neg) in the same process reads "
@@ -117,7 +122,7 @@ def cmd_traffic(args) -> str:
         f"| write bytes per launch | {we / 1e6:.1f} MB |",
         f"| algorithmic bytes per launch (K/V once + Q + out) | {args.algorithmic / 1e6:.1f} MB |" if args.algorithmic else "",
         "",
-        f"source_sha256: {source_sha()}",
+        f"source_sha256: {source_sha(SOURCES[args.kernel])}",
         f"hbm_bytes_per_launch: {int(fe + we)}",
         f"fetch_bytes_per_launch: {int(fe)}",
         f"write_bytes_per_launch: {int(we)}",
@@ -158,6 +163,7 @@ def main():
     sub = ap.add_subparsers(dest="what", required=True)
     s = sub.add_parser("stats"); s.add_argument("csv")
     t = sub.add_parser("traffic"); t.add_argument("--fetch", required=True); t.add_argument("--write", required=True)
+    t.add_argument("--kernel", default=EXTEND_KERNEL, choices=sorted(SOURCES))
     t.add_argument("--copy-mib", type=int, required=True); t.add_argument("--algorithmic", type=float, default=0)
     c = sub.add_parser("counters"); c.add_argument("csv", nargs="+"); c.add_argument("--kernel", default=EXTEND_KERNEL)
     for p in (s, t, c):
