@@ -118,6 +118,9 @@ def main():
     ap.add_argument("--workload", default="react_128k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cascade", action="store_true",
+                    help="for a workload whose sequences share a prefix (forked_agents), run the cascade extend "
+                         "(shared keys once for the whole batch, then the private keys, then an LSE merge)")
     ap.add_argument("--cold-mib", type=int, default=0,
                     help="write a scratch buffer of this size before every step, outside the timed "
                          "region, so the step starts with cold caches; times then come from HIP events")
@@ -159,8 +162,18 @@ def main():
     decode = w.name.startswith("decode")
     attn_bytes = kv_bytes(w.prefix_len, w.suffix_len, w.num_kv_heads, D, elem) + 2 * w.total_tokens * Hq * D * elem
     out = torch.empty_like(d["q"])
+    shared = 0
+    if args.cascade:
+        from paper_2609_39819_amd.workloads import config_shapes
+        shared = int(config_shapes(w.name).get("shared_prefix", 0))
+        if not shared:
+            print(f"--cascade needs a workload with a shared prefix; {w.name} has none", file=sys.stderr)
+            sys.exit(2)
     if decode:
         need = kvt.decode_workspace_bytes(d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, Hq)
+    elif shared:
+        need = kvt.cascade_workspace_bytes(d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.suffix_len,
+                                           shared, Hq)
     else:
         need = kvt.extend_workspace_bytes(d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.suffix_len, Hq)
     ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev) if need else None
@@ -175,6 +188,9 @@ def main():
         if decode:
             kvt.decode_attention(d["q"], d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.scale,
                                  out=out, workspace=ws, use_workspace=need > 0)
+        elif shared:
+            kvt.cascade_extend_attention(d["q"], d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len,
+                                         w.suffix_len, shared, w.scale, out=out, workspace=ws)
         else:
             kvt.extend_attention(d["q"], d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.suffix_len,
                                  w.scale, out=out, workspace=ws, use_workspace=need > 0)
@@ -234,7 +250,7 @@ def main():
         },
         "new_tokens_per_s": w.total_tokens / (ms_per_step * 1e-3),
         "pct_bf16_peak": 100.0 * value / PEAK_BF16_TFLOPS,
-        "attention_kernel": "decode" if decode else "extend",
+        "attention_kernel": "decode" if decode else ("cascade extend" if shared else "extend"),
         "extend_ms": ext_avg,
         "extend_ms_median": float(np.median(ext_ms)),
         "extend_ms_min": float(ext_ms.min()),

@@ -129,6 +129,36 @@ kvt_status kvt_extend_attention(const kvt_pool* pool, const kvt_seqs* seqs,
 size_t kvt_extend_workspace_bytes(const kvt_pool* pool, const kvt_seqs* seqs, int32_t num_q_heads);
 
 /*
+ * kvt_cascade_extend_attention -- kvt_extend_attention for a batch whose
+ * sequences share their first shared_len positions (forked sub-agents reuse
+ * the parent's KV: paper sections 2.1 and 5.2, shared-KV state section 6.1).
+ *
+ * Same result as kvt_extend_attention on the same arguments, computed in
+ * three steps: every new token of the batch attends over the shared keys
+ * [0, shared_len) at once (one pass over the shared pages for the whole
+ * batch), each sequence attends over its private keys [shared_len, P_b + i],
+ * and the two partial results merge by their log-sum-exp weights.
+ *
+ * shared_len: a positive multiple of 16, at most every prefix_len[b]; the
+ * first shared_len/16 block-table entries must be the same pages in every
+ * row (checked mode verifies it; otherwise the result is unspecified).
+ * Violations give KVT_ERR_INVALID_ARG.  workspace: device scratch of at
+ * least kvt_cascade_workspace_bytes() for the same arguments (else
+ * KVT_ERR_WORKSPACE); NULL/0 runs the call as kvt_extend_attention without
+ * a workspace.  Other arguments as for kvt_extend_attention.
+ */
+kvt_status kvt_cascade_extend_attention(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shared_len,
+                                        const void* q, int32_t num_q_heads, float scale,
+                                        void* out, float* lse,
+                                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace of kvt_cascade_extend_attention: (1 + key splits of the private
+ * parts) partial results per row.  0 when the arguments are invalid.
+ * Host-only; enqueues nothing. */
+size_t kvt_cascade_workspace_bytes(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shared_len,
+                                   int32_t num_q_heads);
+
+/*
  * kvt_decode_attention -- one decoding step: attention of each sequence's
  * single new token over its whole cache (paper section 5.2: once a request's
  * prefill completes, LLM decoding proceeds token by token over the same KV).

@@ -168,6 +168,39 @@ ExtendPlan make_decode_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t 
   return p;
 }
 
+// A shared prefix: a positive multiple of 16 no longer than any sequence's
+// prefix; in checked mode every table row must list the same pages for it.
+kvt_status check_shared(const kvt_seqs* seqs, int32_t shared_len) {
+  if (shared_len < kvt::kBlock || shared_len % kvt::kBlock != 0) return KVT_ERR_INVALID_ARG;
+  for (int b = 0; b < seqs->num_seqs; ++b)
+    if (seqs->prefix_len[b] < shared_len) return KVT_ERR_INVALID_ARG;
+  if (seqs->block_table_host != nullptr) {
+    const int32_t* row0 = seqs->block_table_host;
+    for (int b = 1; b < seqs->num_seqs; ++b)
+      if (std::memcmp(row0, seqs->block_table_host + (int64_t)b * seqs->max_blocks,
+                      sizeof(int32_t) * (shared_len / kvt::kBlock)) != 0)
+        return KVT_ERR_INVALID_ARG;
+  }
+  return KVT_OK;
+}
+
+// Cascade: the split plan of the private parts (prefix lengths less the
+// shared prefix); the workspace holds 1 + nsplit partials per row.
+ExtendPlan cascade_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shared_len, int32_t num_q_heads,
+                        int64_t T) {
+  std::vector<int32_t> priv(seqs->num_seqs);
+  for (int b = 0; b < seqs->num_seqs; ++b) priv[b] = seqs->prefix_len[b] - shared_len;
+  kvt_seqs ps = *seqs;
+  ps.prefix_len = priv.data();
+  ExtendPlan p = make_plan(pool, &ps, num_q_heads, T);
+  const int64_t rows = T * num_q_heads;
+  const int nparts = 1 + p.nsplit;
+  const size_t o_bytes = (size_t)nparts * rows * pool->head_dim * sizeof(float);
+  const size_t ml_bytes = (size_t)nparts * rows * 2 * sizeof(float);
+  p.ws_bytes = ((o_bytes + 255) / 256) * 256 + ml_bytes;
+  return p;
+}
+
 // out must not overlap q or a pool; lse must not overlap out.
 kvt_status check_outputs(const kvt_pool* pool, const void* q, int32_t num_q_heads, const void* out,
                          const float* lse, int64_t T) {
@@ -199,6 +232,10 @@ kvt::ExtendArgs base_args(const kvt_pool* pool, const kvt_seqs* seqs, const void
   a.num_kv_heads = pool->num_kv_heads;
   a.group = num_q_heads / pool->num_kv_heads;
   a.scale_log2 = scale * 1.4426950408889634f;
+  a.kbeg = 0;
+  a.kend = INT32_MAX;
+  a.direct = plan.nsplit == 1 ? 1 : 0;
+  a.part_base = 0;
   a.nsplit = plan.nsplit;
   a.total_rows = (int32_t)T;
   if (plan.nsplit > 1) {
@@ -350,6 +387,82 @@ kvt_status kvt_extend_attention(const kvt_pool* pool, const kvt_seqs* seqs, cons
     if (e != hipSuccess) return device_error(e);
   }
   return plan.nsplit > 1 ? combine(a, pool, out, lse, T, num_q_heads, plan.nsplit, s) : KVT_OK;
+}
+
+size_t kvt_cascade_workspace_bytes(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shared_len,
+                                   int32_t num_q_heads) {
+  if (check_pool(pool) != KVT_OK) return 0;
+  int64_t T = 0;
+  if (check_seqs(seqs, &T) != KVT_OK) return 0;
+  if (num_q_heads < 1 || num_q_heads % pool->num_kv_heads != 0) return 0;
+  if (check_shared(seqs, shared_len) != KVT_OK) return 0;
+  return cascade_plan(pool, seqs, shared_len, num_q_heads, T).ws_bytes;
+}
+
+kvt_status kvt_cascade_extend_attention(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shared_len,
+                                        const void* q, int32_t num_q_heads, float scale, void* out, float* lse,
+                                        void* workspace, size_t workspace_bytes, void* stream) {
+  kvt_status st = check_pool(pool);
+  if (st != KVT_OK) return st;
+  int64_t T = 0;
+  if ((st = check_seqs(seqs, &T)) != KVT_OK) return st;
+  if ((st = check_shared(seqs, shared_len)) != KVT_OK) return st;
+  if (workspace == nullptr && workspace_bytes == 0)   // no scratch: the plain extend computes the same
+    return kvt_extend_attention(pool, seqs, q, num_q_heads, scale, out, lse, nullptr, 0, stream);
+  if (q == nullptr || out == nullptr) return KVT_ERR_INVALID_ARG;
+  if (num_q_heads < 1 || num_q_heads % pool->num_kv_heads != 0) return KVT_ERR_INVALID_ARG;
+  if (!(scale > 0.f) || !std::isfinite(scale)) return KVT_ERR_INVALID_ARG;
+  if ((st = check_table_ids(pool, seqs)) != KVT_OK) return st;
+  if ((st = check_outputs(pool, q, num_q_heads, out, lse, T)) != KVT_OK) return st;
+  const ExtendPlan plan = cascade_plan(pool, seqs, shared_len, num_q_heads, T);
+  if (workspace == nullptr || workspace_bytes < plan.ws_bytes) return KVT_ERR_WORKSPACE;
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const int G = num_q_heads / pool->num_kv_heads;
+  const int nparts = 1 + plan.nsplit;
+  ExtendPlan parts = plan;
+  parts.nsplit = nparts;                       // partial buffers hold the shared part + the splits
+  kvt::ExtendArgs a = base_args(pool, seqs, q, num_q_heads, scale, out, lse, T, parts, workspace);
+  a.direct = 0;
+
+  // shared part: every new token of the batch against keys [0, shared_len),
+  // all of them visible (one virtual sequence whose causal limits start at
+  // shared_len - 1), read through the first sequence's table row
+  a.nsplit = 1;
+  a.part_base = 0;
+  a.kbeg = 0;
+  a.kend = shared_len;
+  a.nseq = 1;
+  a.seq[0] = kvt::SeqDesc{plan.order[0], shared_len - 1, (int32_t)T, 0};
+  a.unit_begin[0] = 0;
+  a.unit_begin[1] = row_tiles((int32_t)T, G);
+  hipError_t e = kvt::launch_extend(a, pool->dtype, pool->head_dim, a.unit_begin[1] * pool->num_kv_heads, s);
+  if (e != hipSuccess) return device_error(e);
+
+  // private parts: each sequence over keys [shared_len, P_b + i], causal
+  std::vector<int32_t> row_off(seqs->num_seqs + 1, 0);
+  for (int b = 0; b < seqs->num_seqs; ++b) row_off[b + 1] = row_off[b] + seqs->suffix_len[b];
+  a.nsplit = plan.nsplit;
+  a.part_base = 1;
+  a.kbeg = shared_len;
+  a.kend = INT32_MAX;
+  for (size_t c0 = 0; c0 < plan.order.size(); c0 += kvt::kSeqsPerLaunch) {
+    const int n = (int)std::min<size_t>(kvt::kSeqsPerLaunch, plan.order.size() - c0);
+    a.nseq = n;
+    int32_t units = 0;
+    for (int i = 0; i < n; ++i) {
+      const int b = plan.order[c0 + i];
+      a.seq[i] = kvt::SeqDesc{b, seqs->prefix_len[b], seqs->suffix_len[b], row_off[b]};
+      a.unit_begin[i] = units;
+      units += row_tiles(seqs->suffix_len[b], G) * plan.nsplit;
+    }
+    a.unit_begin[n] = units;
+    const int64_t grid = (int64_t)units * pool->num_kv_heads;
+    if (grid > INT32_MAX) return KVT_ERR_INVALID_ARG;
+    e = kvt::launch_extend(a, pool->dtype, pool->head_dim, (int)grid, s);
+    if (e != hipSuccess) return device_error(e);
+  }
+  return combine(a, pool, out, lse, T, num_q_heads, nparts, s);
 }
 
 size_t kvt_decode_workspace_bytes(const kvt_pool* pool, const kvt_seqs* seqs, int32_t num_q_heads) {

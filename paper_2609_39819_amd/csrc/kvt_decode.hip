@@ -273,11 +273,11 @@ __global__ __launch_bounds__(kWaves * 64) void decode_kernel(const ExtendArgs a)
       }
     }
     const int64_t row = (int64_t)sd.row_off * a.num_q_heads + g * G + r;
-    if (a.nsplit == 1) {
+    if (a.direct) {
       store1(reinterpret_cast<T*>(a.out) + row * D + d, acc / lsum);
       if (a.lse != nullptr && d == 0) a.lse[row] = (mstar + __builtin_log2f(lsum)) * kLn2;
     } else {
-      const int64_t prow = (int64_t)split * a.total_rows * a.num_q_heads + row;
+      const int64_t prow = (int64_t)(a.part_base + split) * a.total_rows * a.num_q_heads + row;
       a.part_o[prow * D + d] = acc;
       if (d == 0) {
         a.part_ml[prow * 2] = mstar;

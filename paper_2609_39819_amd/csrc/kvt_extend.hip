@@ -83,17 +83,19 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
   const int split = local % a.nsplit;
   const int r0 = rt * kExtTileRows;
   const int P = sd.prefix;
-  const int L = P + sd.suffix;
+  const int L = min(P + sd.suffix, a.kend);      // positions that can be read
   const int nblk = (L + kBlock - 1) / kBlock;
 
-  // keys this tile needs: up to the last query's own position
+  // keys this tile needs: from kbeg up to the last query's own position
+  // (or kend); the range is split evenly over the key splits
   const int t_last = min(sd.suffix - 1, (r0 + kExtTileRows - 1) / G);
-  const int kmax = P + t_last + 1;
+  const int kmax = min(P + t_last + 1, a.kend);
   const int ntiles_kv = (kmax + KT - 1) / KT;
-  const int per_split = (ntiles_kv + a.nsplit - 1) / a.nsplit;
-  const int j0 = split * per_split;
+  const int jlo = a.kbeg / KT;
+  const int per_split = (ntiles_kv - jlo + a.nsplit - 1) / a.nsplit;
+  const int j0 = jlo + split * per_split;
   const int j1 = min(ntiles_kv, j0 + per_split);
-  const int lim_min = P + r0 / G;   // smallest causal limit of the tile
+  const int lim_min = min(P + r0 / G, a.kend - 1);   // smallest last-visible key of the tile
 
   // ---- this lane's query rows: block b = rows kExtRowsPerWave*wave + 32*b + l32
   int lim[NB];
@@ -106,7 +108,7 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
     if (!row_valid[b]) r = rows_seq - 1;
     const int t = r / G;
     const int h = g * G + (r - t * G);
-    lim[b] = P + t;                                     // last visible position
+    lim[b] = min(P + t, a.kend - 1);                    // last visible position
     qrow[b] = (int64_t)(sd.row_off + t) * a.num_q_heads + h;
   }
   bf16x8 qreg[NB][KSTEPS];
@@ -241,6 +243,15 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
             if (kabs > lim[b]) s[b][half][e] = -INFINITY;
           }
     }
+    if (j * KT < a.kbeg) {   // first tile of a range that starts inside it
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int half = 0; half < 2; ++half)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            if (j * KT + half * 32 + 8 * (e >> 2) + 4 * hh + (e & 3) < a.kbeg) s[b][half][e] = -INFINITY;
+    }
     float alpha[NB];
     bool moved = false;
 #pragma unroll
@@ -348,7 +359,7 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
   for (int b = 0; b < NB; ++b) {
     const float l_tot = pair_sum(l_run[b]);
     if (!row_valid[b]) continue;
-    if (a.nsplit == 1) {
+    if (a.direct) {
       const float inv = 1.0f / l_tot;
       T* op = reinterpret_cast<T*>(a.out) + qrow[b] * D;
 #pragma unroll
@@ -361,7 +372,7 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
         }
       if (a.lse != nullptr && hh == 0) a.lse[qrow[b]] = (m_ref[b] + __builtin_log2f(l_tot)) * kLn2;
     } else {
-      const int64_t prow = (int64_t)split * a.total_rows * a.num_q_heads + qrow[b];
+      const int64_t prow = (int64_t)(a.part_base + split) * a.total_rows * a.num_q_heads + qrow[b];
       float* op = a.part_o + prow * D;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)

@@ -63,6 +63,10 @@ struct ExtendArgs {
   int32_t num_kv_heads;
   int32_t group;        // Hq / Hkv
   float scale_log2;     // scale * log2(e)
+  int32_t kbeg;         // first key position attended (multiple of 16; 0 = from the start)
+  int32_t kend;         // key positions >= kend are not attended (INT32_MAX = no cap)
+  int32_t direct;       // 1: write out/lse; 0: write partial (part_base + split)
+  int32_t part_base;    // first partial slot of this launch
   int32_t nsplit;
   int32_t total_rows;   // T of the whole call
   int32_t nseq;

@@ -27,7 +27,8 @@ KVT_DTYPE_BF16 = 0
 KVT_DTYPE_F32 = 1
 BLOCK_SIZE = 16
 
-EXPORTED = ("kvt_append_kv", "kvt_decode_attention", "kvt_decode_workspace_bytes", "kvt_extend_attention",
+EXPORTED = ("kvt_append_kv", "kvt_cascade_extend_attention", "kvt_cascade_workspace_bytes",
+            "kvt_decode_attention", "kvt_decode_workspace_bytes", "kvt_extend_attention",
             "kvt_extend_workspace_bytes", "kvt_last_hip_error", "kvt_status_str")
 
 
@@ -68,6 +69,12 @@ def lib():
         L.kvt_extend_attention.restype = ctypes.c_int
         L.kvt_extend_workspace_bytes.argtypes = [P(KvtPool), P(KvtSeqs), ctypes.c_int32]
         L.kvt_extend_workspace_bytes.restype = ctypes.c_size_t
+        L.kvt_cascade_extend_attention.argtypes = [P(KvtPool), P(KvtSeqs), ctypes.c_int32, ctypes.c_void_p,
+                                                   ctypes.c_int32, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p,
+                                                   ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+        L.kvt_cascade_extend_attention.restype = ctypes.c_int
+        L.kvt_cascade_workspace_bytes.argtypes = [P(KvtPool), P(KvtSeqs), ctypes.c_int32, ctypes.c_int32]
+        L.kvt_cascade_workspace_bytes.restype = ctypes.c_size_t
         L.kvt_decode_attention.argtypes = L.kvt_extend_attention.argtypes
         L.kvt_decode_attention.restype = ctypes.c_int
         L.kvt_decode_workspace_bytes.argtypes = L.kvt_extend_workspace_bytes.argtypes
@@ -185,6 +192,25 @@ def extend_attention(q, k_pool, v_pool, block_table, prefix_len: Sequence[int], 
                       prefix_len, suffix_len, scale, out, lse, return_lse, workspace, use_workspace, stream, checked)
 
 
+def cascade_workspace_bytes(k_pool, v_pool, block_table, prefix_len, suffix_len, shared_len: int,
+                            num_q_heads: int) -> int:
+    pool = _pool_struct(k_pool, v_pool)
+    seqs = _seqs(prefix_len, suffix_len, block_table, False)
+    return int(lib().kvt_cascade_workspace_bytes(ctypes.byref(pool), ctypes.byref(seqs.struct), int(shared_len),
+                                                 int(num_q_heads)))
+
+
+def cascade_extend_attention(q, k_pool, v_pool, block_table, prefix_len, suffix_len, shared_len: int,
+                             scale: Optional[float] = None, *, out=None, lse=None, return_lse: bool = False,
+                             workspace=None, use_workspace: bool = True, stream=None, checked: bool = False):
+    """Extend attention for sequences that share their first ``shared_len``
+    positions (``kvt_cascade_extend_attention``); same result as
+    ``extend_attention``."""
+    return _attention("kvt_cascade_extend_attention", "kvt_cascade_workspace_bytes", q, k_pool, v_pool,
+                      block_table, prefix_len, suffix_len, scale, out, lse, return_lse, workspace, use_workspace,
+                      stream, checked, shared=int(shared_len))
+
+
 def decode_workspace_bytes(k_pool, v_pool, block_table, prefix_len, num_q_heads: int) -> int:
     pool = _pool_struct(k_pool, v_pool)
     seqs = _seqs(prefix_len, np.ones(len(prefix_len), dtype=np.int32), block_table, False)
@@ -203,8 +229,9 @@ def decode_attention(q, k_pool, v_pool, block_table, prefix_len: Sequence[int], 
 
 
 def _attention(entry: str, ws_entry: str, q, k_pool, v_pool, block_table, prefix_len, suffix_len, scale, out, lse,
-               return_lse, workspace, use_workspace, stream, checked):
+               return_lse, workspace, use_workspace, stream, checked, shared: Optional[int] = None):
     import torch
+    lead = () if shared is None else (shared,)   # the cascade entry points take shared_len after seqs
     pool = _pool_struct(k_pool, v_pool)
     seqs = _seqs(prefix_len, suffix_len, block_table, checked)
     T = int(np.sum(np.asarray(suffix_len, dtype=np.int64)))
@@ -225,11 +252,11 @@ def _attention(entry: str, ws_entry: str, q, k_pool, v_pool, block_table, prefix
     if workspace is not None:
         ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
     elif use_workspace:
-        need = int(getattr(lib(), ws_entry)(ctypes.byref(pool), ctypes.byref(seqs.struct), Hq))
+        need = int(getattr(lib(), ws_entry)(ctypes.byref(pool), ctypes.byref(seqs.struct), *lead, Hq))
         if need:
             workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
             ws_ptr, ws_bytes = workspace.data_ptr(), need
-    st = getattr(lib(), entry)(ctypes.byref(pool), ctypes.byref(seqs.struct), q.data_ptr(), Hq, float(scale),
+    st = getattr(lib(), entry)(ctypes.byref(pool), ctypes.byref(seqs.struct), *lead, q.data_ptr(), Hq, float(scale),
                                out.data_ptr(), lse.data_ptr() if lse is not None else None, ws_ptr, ws_bytes,
                                _stream_handle(q.device, stream))
     if st != KVT_OK:

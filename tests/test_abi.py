@@ -146,6 +146,33 @@ def test_decode_specific_checks():
     assert _decode(_pool(), _seqs(S=(1,), host=host)) == kvt.KVT_ERR_OUT_OF_RANGE
 
 
+def _cascade(pool, seqs, shared, hq=4, scale=0.125, q=FAKE_Q, out=FAKE_OUT, ws=None, ws_bytes=0):
+    return kvt.lib().kvt_cascade_extend_attention(ctypes.byref(pool), ctypes.byref(seqs.struct), shared, q, hq,
+                                                  scale, out, None, ws, ws_bytes, None)
+
+
+@no_gpu_only
+def test_cascade_specific_checks():
+    E = kvt.KVT_ERR_INVALID_ARG
+    two = _seqs(P=(240, 100), S=(16, 16), max_blocks=16)
+    for bad in (0, 8, 17, 112, -16):          # not a positive multiple of 16, or longer than a prefix (100)
+        assert _cascade(_pool(), two, bad, ws=0x60000000000, ws_bytes=1 << 30) == E
+    host = np.stack([np.arange(16), np.arange(16, 32)]).astype(np.int32)   # first pages differ
+    assert _cascade(_pool(), _seqs(P=(240, 100), S=(16, 16), max_blocks=16, host=host), 64,
+                    ws=0x60000000000, ws_bytes=1 << 30) == E
+    assert _cascade(_pool(), two, 64, ws=0x60000000000, ws_bytes=16) == kvt.KVT_ERR_WORKSPACE
+
+
+def test_cascade_workspace_bytes():
+    pool = _pool(nb=1 << 20, hkv=8, d=128)
+    s = _seqs(P=(8192, 20000), S=(2048, 1000), max_blocks=2048)
+    ws = kvt.lib().kvt_cascade_workspace_bytes(ctypes.byref(pool), ctypes.byref(s.struct), 4096, 96)
+    rows = 3048 * 96
+    parts = ws // (rows * (128 + 2) * 4)       # 1 + key splits of the private parts
+    assert parts >= 2 and ws == -(-parts * rows * 128 * 4 // 256) * 256 + parts * rows * 2 * 4
+    assert kvt.lib().kvt_cascade_workspace_bytes(ctypes.byref(pool), ctypes.byref(s.struct), 4100, 96) == 0
+
+
 def test_decode_workspace_bytes_follow_the_split_plan():
     def ws(pool, seqs, hq):
         return kvt.lib().kvt_decode_workspace_bytes(ctypes.byref(pool), ctypes.byref(seqs.struct), hq)

@@ -1,0 +1,87 @@
+"""Cascade extend (``kvt_cascade_extend_attention``) against the fp64 oracle.
+
+The cascade computes the same attention as extend (shared keys for the whole
+batch at once, private keys per sequence, log-sum-exp merge), so the
+reference is ``oracle_extend``.  Covered: the forked-agents workload (4096
+shared positions, 16 sequences; sampled rows, lse, agreement with the plain
+extend kernel) and edge shapes: a shared length that is not a multiple of the
+64-key tile, a sequence whose whole prefix is shared, a single sequence,
+D = 64, fp32 storage, and key splits in the private parts.
+"""
+import numpy as np
+import pytest
+
+from oracle import oracle_append, oracle_extend
+from paper_2609_39819_amd import kvt
+from paper_2609_39819_amd.workloads import build_workload, config_shapes
+
+from gpu_common import (cached_config, compare, gather_rows, oracle_pools, run_append, run_extend, sample_rows, say,
+                        stage, to_f64)
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    torch.cuda.set_device(0)
+    yield
+    torch.cuda.synchronize()
+
+
+def run_cascade(w, d, shared, **kw):
+    say(f"kvt_cascade_extend_attention {w.name}/{w.variant} shared={shared} {kw if kw else ''}")
+    r = kvt.cascade_extend_attention(d["q"], d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len,
+                                     w.suffix_len, shared, w.scale, **kw)
+    torch.cuda.synchronize()
+    return r
+
+
+@pytest.mark.timeout(900)
+def test_forked_agents_cascade_matches_oracle():
+    w = cached_config("forked_agents")
+    shared = config_shapes("forked_agents")["shared_prefix"]
+    d = stage(w)
+    run_append(w, d)
+    out, lse = run_cascade(w, d, shared, return_lse=True)
+    rows = sample_rows(w, 6)
+    kp, vp = oracle_pools("forked_agents")
+    ref_o, ref_l = oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len, w.suffix_len, w.num_kv_heads, w.scale,
+                                 rows=rows)
+    compare(gather_rows(to_f64(out, w.dtype), w, rows), ref_o, "forked cascade out")
+    compare(gather_rows(lse.cpu().numpy().astype(np.float64), w, rows), ref_l, "forked cascade lse")
+    assert bool(torch.isfinite(out.float()).all())
+    plain = run_extend(w, d)
+    compare(to_f64(out, w.dtype), to_f64(plain, w.dtype), "cascade vs extend", max_abs=1e-2, mean_abs=5e-4)
+    del d
+    torch.cuda.empty_cache()
+
+
+CASC_EDGE = [
+    # (prefix lengths, suffix lengths, shared, Hq, Hkv, D, dtype)
+    ([200, 500, 96], [40, 300, 7], 48, 12, 1, 128, "bf16"),          # shared not a multiple of 64
+    ([4096, 6000], [100, 2048], 4096, 12, 2, 128, "bf16"),            # one prefix entirely shared
+    ([9000], [513], 1024, 8, 2, 128, "bf16"),                         # a single sequence
+    ([3000, 2000, 2500], [64, 65, 63], 1600, 16, 8, 64, "bf16"),      # D = 64
+    ([700, 900], [33, 40], 320, 4, 1, 64, "f32"),                     # fp32 storage
+    ([40000, 33000], [16, 20], 16384, 8, 8, 128, "bf16"),             # short suffixes: private parts split
+]
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("case", range(len(CASC_EDGE)))
+def test_cascade_edge_shapes(case):
+    P, S, shared, Hq, Hkv, D, dt = CASC_EDGE[case]
+    w = build_workload(name=f"casc_edge{case}", seed=800 + case, prefix_len=P, suffix_len=S, num_q_heads=Hq,
+                       num_kv_heads=Hkv, head_dim=D, dtype=dt, num_blocks=16384, shared_prefix_blocks=shared // 16)
+    d = stage(w)
+    run_append(w, d, checked=True)
+    out, lse = run_cascade(w, d, shared, return_lse=True, checked=True)
+    kp, vp = oracle_append(w.k_pool_c, w.v_pool_c, w.compact_table, w.prefix_len, w.suffix_len, w.k_new, w.v_new)
+    ref_o, ref_l = oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len, w.suffix_len, Hkv, w.scale)
+    compare(to_f64(out, dt), ref_o, f"casc_edge{case} out")
+    compare(lse.cpu().numpy().astype(np.float64), ref_l, f"casc_edge{case} lse")
+    del d
+    torch.cuda.empty_cache()
