@@ -25,6 +25,7 @@ sys.path.insert(0, ROOT)
 METRIC = "extend-attention TFLOP/s and new tokens/s at 128K reused prefix; % bf16 MFMA peak"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X published dense bf16 MFMA peak
 PEAK_HBM_GBPS = 8000.0      # MI355X published HBM3E bandwidth
+PEAK_HOST_LINK_GBPS = 64.0  # PCIe 5.0 x16, one direction
 
 
 def log(*a):
@@ -110,6 +111,48 @@ def sample_power(step, ms_per_step: float):
             "gfx_clock_mhz": clocks or None, "source": "amd-smi metric -p -c"}
 
 
+def bench_copy(args, w, d, dev):
+    """Offload every used page of the workload to pinned host memory and
+    reload it into the same pages; HIP events around each launch."""
+    import torch
+    from paper_2609_39819_amd import kvt
+    ids = torch.from_numpy(np.ascontiguousarray(w.phys_ids, dtype=np.int32)).to(dev)
+    n = int(ids.numel())
+    host = torch.empty((n, 2) + tuple(d["k_pool"].shape[1:]), dtype=d["k_pool"].dtype, pin_memory=True)
+    nbytes = host.numel() * host.element_size()
+    stream = torch.cuda.current_stream(dev)
+    for _ in range(args.warmup):
+        kvt.copy_blocks(d["k_pool"], d["v_pool"], ids, host, to_host=True)
+        kvt.copy_blocks(d["k_pool"], d["v_pool"], ids, host, to_host=False)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    for e in evs:
+        e[0].record(stream)
+        kvt.copy_blocks(d["k_pool"], d["v_pool"], ids, host, to_host=True)
+        e[1].record(stream)
+        kvt.copy_blocks(d["k_pool"], d["v_pool"], ids, host, to_host=False)
+        e[2].record(stream)
+    torch.cuda.synchronize()
+    off = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
+    rel = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
+    log(f"{n} pages, {nbytes / 1e6:.1f} MB: offload {off:.3f} ms ({nbytes / off / 1e6:.1f} GB/s), "
+        f"reload {rel:.3f} ms ({nbytes / rel / 1e6:.1f} GB/s)")
+    step_ms = off + rel
+    return {
+        "metric": "HBM <-> pinned-host page moves (offload + reload of every page of the workload)",
+        "value": 2 * nbytes / (step_ms * 1e-3) / 1e9, "unit": "GB/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": step_ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "u8", "data": "synthetic",
+        "config": {"workload": f"{w.name} pages", "pages": n, "bytes_each_way": nbytes},
+        "offload_ms": off, "reload_ms": rel,
+        "offload_gbps": nbytes / (off * 1e-3) / 1e9, "reload_gbps": nbytes / (rel * 1e-3) / 1e9,
+        "roofline": {"bound": "host link", "achieved": 2 * nbytes / (step_ms * 1e-3) / 1e9,
+                     "peak": PEAK_HOST_LINK_GBPS, "unit": "GB/s",
+                     "frac": 2 * nbytes / (step_ms * 1e-3) / 1e9 / PEAK_HOST_LINK_GBPS, "traffic": None},
+        "gpu": torch.cuda.get_device_name(dev),
+    }
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -121,6 +164,9 @@ def main():
     ap.add_argument("--cascade", action="store_true",
                     help="for a workload whose sequences share a prefix (forked_agents), run the cascade extend "
                          "(shared keys once for the whole batch, then the private keys, then an LSE merge)")
+    ap.add_argument("--copy", action="store_true",
+                    help="instead of attention, time moving every page of the workload to pinned host memory "
+                         "and back (kvt_copy_blocks)")
     ap.add_argument("--cold-mib", type=int, default=0,
                     help="write a scratch buffer of this size before every step, outside the timed "
                          "region, so the step starts with cold caches; times then come from HIP events")
@@ -153,6 +199,9 @@ def main():
     d = stage_on_device(w, dev)
     torch.cuda.synchronize()
 
+    if args.copy:
+        print(json.dumps(bench_copy(args, w, d, dev)), flush=True)
+        return
     Hq, D = w.num_q_heads, w.head_dim
     flops = algorithmic_flops(w.prefix_len, w.suffix_len, Hq, D)
     elem = 2 if w.dtype == "bf16" else 4

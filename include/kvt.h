@@ -188,6 +188,35 @@ kvt_status kvt_decode_attention(const kvt_pool* pool, const kvt_seqs* seqs,
  * arguments are invalid.  Host-only; enqueues nothing. */
 size_t kvt_decode_workspace_bytes(const kvt_pool* pool, const kvt_seqs* seqs, int32_t num_q_heads);
 
+/* Direction of kvt_copy_blocks. */
+typedef enum {
+  KVT_COPY_TO_HOST = 0,     /* pool pages -> host buffer (offload)  */
+  KVT_COPY_TO_DEVICE = 1    /* host buffer -> pool pages (reload)   */
+} kvt_copy_direction;
+
+/*
+ * kvt_copy_blocks -- move a list of pages between the HBM pools and host
+ * memory (the GPU <-> host tier of the multi-tier KV cache: pages leave HBM
+ * under memory pressure and come back for reuse; paper sections 6 and 7).
+ *
+ * For i < num_ids, with page = block_ids[i]:
+ *   KVT_COPY_TO_HOST:   host[i][0] = K pool page, host[i][1] = V pool page
+ *   KVT_COPY_TO_DEVICE: the reverse
+ * where host is a packed [num_ids][2][Hkv][16][D] array of the pool dtype.
+ *
+ * block_ids: DEVICE int32 [num_ids].  block_ids_host: optional HOST mirror;
+ * when given, every id must lie in [0, num_blocks) and, for
+ * KVT_COPY_TO_DEVICE, appear once (else KVT_ERR_OUT_OF_RANGE).  Without it an
+ * id outside the pool is skipped (never dereferenced).
+ * host: pinned host memory allocated through HIP (hipHostMalloc or
+ * equivalent), at least num_ids * 2 * Hkv * 16 * D * elem bytes; other
+ * memory gives KVT_ERR_INVALID_ARG.  The GPU reads/writes it directly over
+ * the host link; it must stay allocated until the stream passes the call.
+ * num_ids = 0 is a no-op.  Enqueued on `stream`; nothing is allocated.
+ */
+kvt_status kvt_copy_blocks(const kvt_pool* pool, const int32_t* block_ids, const int32_t* block_ids_host,
+                           int64_t num_ids, void* host, int32_t direction, void* stream);
+
 /* Static English text for a status code (never NULL). */
 const char* kvt_status_str(kvt_status s);
 

@@ -20,6 +20,9 @@ What it computes (the problem the paper frames and the definition it implies):
   sum of values.
 * ``brute_force_extend`` -- the same definition in pure-Python loops over the
   un-paged logical sequence, used to pin ``oracle_extend`` on tiny inputs.
+* ``oracle_to_host`` / ``oracle_to_device`` -- whole pages moved between the
+  HBM tier and a packed host buffer (tiered cache, §6; local GPU <-> CPU
+  engine, §7): a bitwise copy in page-list order.
 
 Every function here is pinned by ``tests/test_oracle_pins.py`` against brute
 force, closed forms, a library routine and invariants; none is
@@ -32,3 +35,4 @@ from .attention import (  # noqa: F401
     brute_force_extend,
     gather_logical,
 )
+from .blocks import oracle_to_device, oracle_to_host  # noqa: F401

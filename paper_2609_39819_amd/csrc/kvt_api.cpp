@@ -389,6 +389,49 @@ kvt_status kvt_extend_attention(const kvt_pool* pool, const kvt_seqs* seqs, cons
   return plan.nsplit > 1 ? combine(a, pool, out, lse, T, num_q_heads, plan.nsplit, s) : KVT_OK;
 }
 
+kvt_status kvt_copy_blocks(const kvt_pool* pool, const int32_t* block_ids, const int32_t* block_ids_host,
+                           int64_t num_ids, void* host, int32_t direction, void* stream) {
+  kvt_status st = check_pool(pool);
+  if (st != KVT_OK) return st;
+  if (num_ids < 0 || (num_ids > 0 && (block_ids == nullptr || host == nullptr))) return KVT_ERR_INVALID_ARG;
+  if (direction != KVT_COPY_TO_HOST && direction != KVT_COPY_TO_DEVICE) return KVT_ERR_INVALID_ARG;
+  if (num_ids == 0) return KVT_OK;
+  const int64_t page_bytes = (int64_t)pool->num_kv_heads * kvt::kBlock * pool->head_dim * elem_bytes(pool->dtype);
+  if (num_ids > (INT64_MAX / 4) / (2 * page_bytes)) return KVT_ERR_INVALID_ARG;
+  if (block_ids_host != nullptr) {
+    std::unordered_set<int32_t> seen;
+    for (int64_t i = 0; i < num_ids; ++i) {
+      const int32_t id = block_ids_host[i];
+      if (id < 0 || id >= pool->num_blocks) return KVT_ERR_OUT_OF_RANGE;
+      // two host pages landing on one pool page would race
+      if (direction == KVT_COPY_TO_DEVICE && !seen.insert(id).second) return KVT_ERR_OUT_OF_RANGE;
+    }
+  }
+  // the host side must be pinned memory the device can address
+  hipPointerAttribute_t attr;
+  std::memset(&attr, 0, sizeof(attr));
+  if (hipPointerGetAttributes(&attr, host) != hipSuccess) {
+    (void)hipGetLastError();
+    return KVT_ERR_INVALID_ARG;
+  }
+  if (attr.type != hipMemoryTypeHost) return KVT_ERR_INVALID_ARG;
+  void* host_dev = attr.devicePointer != nullptr ? attr.devicePointer : host;
+
+  kvt::CopyArgs a;
+  a.k_pool = pool->k;
+  a.v_pool = pool->v;
+  a.ids = block_ids;
+  a.n = num_ids;
+  a.host = host_dev;
+  a.page_bytes = page_bytes;
+  a.num_blocks = pool->num_blocks;
+  a.to_host = direction == KVT_COPY_TO_HOST ? 1 : 0;
+  const int64_t pieces = num_ids * 2 * page_bytes / 16;
+  const int grid = (int)std::min<int64_t>((pieces + 255) / 256, 8192);
+  const hipError_t e = kvt::launch_copy_blocks(a, grid, reinterpret_cast<hipStream_t>(stream));
+  return e == hipSuccess ? KVT_OK : device_error(e);
+}
+
 size_t kvt_cascade_workspace_bytes(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shared_len,
                                    int32_t num_q_heads) {
   if (check_pool(pool) != KVT_OK) return 0;

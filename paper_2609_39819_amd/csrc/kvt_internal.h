@@ -83,10 +83,22 @@ struct CombineArgs {
   int32_t nsplit;
 };
 
+struct CopyArgs {
+  void* k_pool;
+  void* v_pool;
+  const int32_t* ids;   // device, n page ids
+  int64_t n;
+  void* host;           // pinned host buffer [n][K|V][page_bytes], device-accessible
+  int64_t page_bytes;   // bytes of one page of one tensor: Hkv * 16 * D * elem
+  int64_t num_blocks;
+  int32_t to_host;      // 1: pool -> host; 0: host -> pool
+};
+
 // Launchers (device code files).  Return the launch status.
 hipError_t launch_append(const AppendArgs& a, int dtype, int head_dim, hipStream_t stream);
 hipError_t launch_extend(const ExtendArgs& a, int dtype, int head_dim, int grid, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs& a, int dtype, int head_dim, hipStream_t stream);
+hipError_t launch_copy_blocks(const CopyArgs& a, int grid, hipStream_t stream);
 // Decode: ExtendArgs with suffix 1 per sequence and nsplit units per sequence.
 hipError_t launch_decode(const ExtendArgs& a, int dtype, int head_dim, int grid, hipStream_t stream);
 

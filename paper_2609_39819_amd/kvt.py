@@ -27,9 +27,11 @@ KVT_DTYPE_BF16 = 0
 KVT_DTYPE_F32 = 1
 BLOCK_SIZE = 16
 
-EXPORTED = ("kvt_append_kv", "kvt_cascade_extend_attention", "kvt_cascade_workspace_bytes",
+EXPORTED = ("kvt_append_kv", "kvt_cascade_extend_attention", "kvt_cascade_workspace_bytes", "kvt_copy_blocks",
             "kvt_decode_attention", "kvt_decode_workspace_bytes", "kvt_extend_attention",
             "kvt_extend_workspace_bytes", "kvt_last_hip_error", "kvt_status_str")
+KVT_COPY_TO_HOST = 0
+KVT_COPY_TO_DEVICE = 1
 
 
 class KvtPool(ctypes.Structure):
@@ -75,6 +77,9 @@ def lib():
         L.kvt_cascade_extend_attention.restype = ctypes.c_int
         L.kvt_cascade_workspace_bytes.argtypes = [P(KvtPool), P(KvtSeqs), ctypes.c_int32, ctypes.c_int32]
         L.kvt_cascade_workspace_bytes.restype = ctypes.c_size_t
+        L.kvt_copy_blocks.argtypes = [P(KvtPool), ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32), ctypes.c_int64,
+                                      ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p]
+        L.kvt_copy_blocks.restype = ctypes.c_int
         L.kvt_decode_attention.argtypes = L.kvt_extend_attention.argtypes
         L.kvt_decode_attention.restype = ctypes.c_int
         L.kvt_decode_workspace_bytes.argtypes = L.kvt_extend_workspace_bytes.argtypes
@@ -209,6 +214,31 @@ def cascade_extend_attention(q, k_pool, v_pool, block_table, prefix_len, suffix_
     return _attention("kvt_cascade_extend_attention", "kvt_cascade_workspace_bytes", q, k_pool, v_pool,
                       block_table, prefix_len, suffix_len, scale, out, lse, return_lse, workspace, use_workspace,
                       stream, checked, shared=int(shared_len))
+
+
+def copy_blocks(k_pool, v_pool, block_ids, host, to_host: bool, *, stream=None, checked: bool = False):
+    """Pages ``block_ids`` (device int32) of the pools to (``to_host``) or from a
+    pinned host tensor [n][2][Hkv][16][D] of the pool dtype (``kvt_copy_blocks``)."""
+    import torch
+    pool = _pool_struct(k_pool, v_pool)
+    if block_ids.dtype != torch.int32 or not block_ids.is_cuda or not block_ids.is_contiguous():
+        raise ValueError("block_ids must be a contiguous int32 device tensor")
+    n = int(block_ids.numel())
+    want = (n, 2) + tuple(k_pool.shape[1:])
+    if tuple(host.shape) != want or host.dtype != k_pool.dtype or not host.is_contiguous():
+        raise ValueError(f"host must be a contiguous {k_pool.dtype} tensor of shape {want}")
+    if n and not host.is_pinned():
+        raise ValueError("host must be pinned memory")
+    ids_host = None
+    if checked:
+        ids_np = np.ascontiguousarray(block_ids.cpu().numpy(), dtype=np.int32)
+        ids_host = ids_np.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+    st = lib().kvt_copy_blocks(ctypes.byref(pool), block_ids.data_ptr() if n else None, ids_host, n,
+                               host.data_ptr() if n else None,
+                               KVT_COPY_TO_HOST if to_host else KVT_COPY_TO_DEVICE,
+                               _stream_handle(k_pool.device, stream))
+    if st != KVT_OK:
+        raise KvtError(st, "kvt_copy_blocks")
 
 
 def decode_workspace_bytes(k_pool, v_pool, block_table, prefix_len, num_q_heads: int) -> int:

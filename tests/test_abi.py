@@ -173,6 +173,31 @@ def test_cascade_workspace_bytes():
     assert kvt.lib().kvt_cascade_workspace_bytes(ctypes.byref(pool), ctypes.byref(s.struct), 4100, 96) == 0
 
 
+def _copy(pool, ids=FAKE_BT, ids_host=None, n=4, host=FAKE_OUT, direction=0):
+    h = None if ids_host is None else np.ascontiguousarray(ids_host, dtype=np.int32).ctypes.data_as(
+        ctypes.POINTER(ctypes.c_int32))
+    return kvt.lib().kvt_copy_blocks(ctypes.byref(pool) if pool is not None else None, ids, h, n, host, direction,
+                                     None)
+
+
+@no_gpu_only
+def test_copy_blocks_checks():
+    E, O = kvt.KVT_ERR_INVALID_ARG, kvt.KVT_ERR_OUT_OF_RANGE
+    assert _copy(_pool(), n=0, ids=None, host=None) == kvt.KVT_OK          # nothing to move
+    assert _copy(None) == E
+    assert _copy(_pool(d=96)) == kvt.KVT_ERR_UNSUPPORTED
+    assert _copy(_pool(), n=-1) == E
+    assert _copy(_pool(), ids=None) == E
+    assert _copy(_pool(), host=None) == E
+    assert _copy(_pool(), direction=2) == E
+    assert _copy(_pool(), ids_host=[0, 1, 64, 2]) == O                      # pool has 64 pages
+    assert _copy(_pool(), ids_host=[0, -1, 3, 2]) == O
+    assert _copy(_pool(), ids_host=[5, 1, 5, 2], direction=1) == O          # one page written twice
+    # host memory that HIP did not pin is refused before anything is enqueued
+    pageable = np.zeros(4 * 2 * 16 * 64, dtype=np.uint16)
+    assert _copy(_pool(), ids_host=[0, 1, 2, 3], host=pageable.ctypes.data) == E
+
+
 def test_decode_workspace_bytes_follow_the_split_plan():
     def ws(pool, seqs, hq):
         return kvt.lib().kvt_decode_workspace_bytes(ctypes.byref(pool), ctypes.byref(seqs.struct), hq)

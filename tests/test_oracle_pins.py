@@ -312,3 +312,43 @@ def test_append_leaves_shared_fork_blocks_alone():
     shared = w.compact_table[0, :2]
     assert np.all(w.compact_table[:, :2] == shared)
     assert np.array_equal(kp[shared], w.k_pool_c[shared]) and np.array_equal(vp[shared], w.v_pool_c[shared])
+
+
+# ---------------------------------------------------------------------------
+# page moves between HBM and host (oracle_to_host / oracle_to_device)
+# ---------------------------------------------------------------------------
+
+def _tiny_pools():
+    # page p, head g, slot s, dim d holds the integer 1000*p + 100*g + 10*s + d
+    nb, hkv, d = 5, 2, 3
+    p, g, s, e = np.meshgrid(np.arange(nb), np.arange(hkv), np.arange(16), np.arange(d), indexing="ij")
+    k = (1000 * p + 100 * g + 10 * s + e).astype(np.float32)
+    return k, -k
+
+
+def test_to_host_packs_pages_in_list_order():
+    from oracle import oracle_to_host
+    k, v = _tiny_pools()
+    host = oracle_to_host(k, v, [3, 0, 3])
+    assert host.shape == (3, 2, 2, 16, 3)
+    assert host[0, 0, 1, 2, 1] == 3000 + 100 + 20 + 1          # K of page 3, head 1, slot 2, dim 1
+    assert host[1, 1, 0, 15, 2] == -(0 + 0 + 150 + 2)          # V of page 0, head 0, slot 15, dim 2
+    assert np.array_equal(host[0], host[2])                    # a page may be read twice
+
+
+def test_to_device_round_trip_and_untouched_pages():
+    from oracle import oracle_to_device, oracle_to_host
+    k, v = _tiny_pools()
+    host = oracle_to_host(k, v, [4, 1])
+    k2, v2 = oracle_to_device(np.zeros_like(k), np.zeros_like(v), [2, 0], host)
+    assert np.array_equal(k2[2], k[4]) and np.array_equal(v2[0], v[1])
+    assert not k2[1].any() and not k2[3].any() and not v2[4].any()    # only listed pages change
+    # offload then reload of the same list is the identity on those pages
+    k3, v3 = oracle_to_device(np.zeros_like(k), np.zeros_like(v), [4, 1], host)
+    assert np.array_equal(k3[[4, 1]], k[[4, 1]]) and np.array_equal(v3[[4, 1]], v[[4, 1]])
+    with pytest.raises(ValueError):
+        oracle_to_device(k, v, [1, 1], host)
+    # bitwise: NaN payloads survive
+    nan_bits = np.array([0x7FC1], dtype=np.uint16)
+    kb = np.zeros((2, 1, 16, 1), dtype=np.uint16); kb[1, 0, 5, 0] = nan_bits[0]
+    assert oracle_to_host(kb, kb, [1])[0, 0, 0, 5, 0] == 0x7FC1
