@@ -37,7 +37,8 @@ def load_traffic(workload: str, decode: bool = False):
     they were taken on the current kernel sources; else None."""
     from paper_2609_39819_amd.profiling import DECODE_SOURCES, EXTEND_SOURCES, read_traffic, source_sha
     kind = "decode" if decode else "extend"
-    t = read_traffic(os.path.join(ROOT, "profiles", f"{kind}_{workload}_traffic.md"))
+    name = workload if workload.startswith(kind) else f"{kind}_{workload}"
+    t = read_traffic(os.path.join(ROOT, "profiles", f"{name}_traffic.md"))
     if t is None or t[0] != source_sha(DECODE_SOURCES if decode else EXTEND_SOURCES):
         return None
     return t[1]
