@@ -217,6 +217,92 @@ typedef enum {
 kvt_status kvt_copy_blocks(const kvt_pool* pool, const int32_t* block_ids, const int32_t* block_ids_host,
                            int64_t num_ids, void* host, int32_t direction, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Host block manager (CPU only; no HIP calls).
+ *
+ * Lifecycle states of message versions (paper section 5.2), the aggregate
+ * state of shared KV (section 6.1), state-prioritized admission
+ * (Algorithm 1) and MRU eviction inside the Suspended tier (section 6.2),
+ * over a pool of num_pages KV pages whose ids it hands out for the block
+ * tables.  A context is an ordered list of messages; a message's current
+ * version has a state and, once it took part in inference, a KV entry of
+ * ceil(tokens / 16) pages.  Forked contexts map their inherited messages to
+ * the parent's entries.  An entry's tier is the strongest state among the
+ * versions that map it: Pinned > Active > Suspended > Discarded (Expired and
+ * Temporary).  Newly written-back entries are admitted in message order:
+ * Temporary-only entries bypass the cache; otherwise the missing pages are
+ * freed from resident entries not read by an in-flight request, Discarded
+ * first (earliest discarded first), then Suspended (most recently suspended
+ * first), then Active (earliest first), then -- for a Pinned newcomer only --
+ * Pinned (earliest first); the newcomer is admitted if that covered it
+ * (entries freed on the way stay freed); entries that changed tier in the
+ * same call rank by creation order.  Pages come from the lowest free ids.
+ * At a request, a message whose entry is gone -- and every later message of
+ * the context -- is a miss and gets a fresh version to recompute.
+ * Not thread-safe: one caller at a time per manager.
+ * ---------------------------------------------------------------------- */
+typedef struct kvt_manager kvt_manager;
+
+/* Lifecycle states as returned by kvt_mgr_message_state. */
+enum { KVT_PINNED = 0, KVT_ACTIVE = 1, KVT_SUSPENDED = 2, KVT_EXPIRED = 3, KVT_TEMPORARY = 4 };
+/* Entry tiers as returned by kvt_mgr_entry_tier. */
+enum { KVT_TIER_PINNED = 0, KVT_TIER_ACTIVE = 1, KVT_TIER_SUSPENDED = 2, KVT_TIER_DISCARDED = 3 };
+
+/* What one request-boundary call did. */
+typedef struct {
+  int64_t admitted_entries, admitted_pages;   /* written back into the cache          */
+  int64_t bypassed_entries;                    /* Temporary KV, not stored             */
+  int64_t rejected_entries;                    /* not enough releasable capacity       */
+  int64_t released_entries, released_pages;    /* evicted or reclaimed to make room    */
+  int64_t hit_tokens, miss_tokens;             /* kvt_mgr_start_prefill: reused / to recompute */
+} kvt_mgr_report;
+
+/* A manager over pages 0 .. num_pages-1 (all free).  NULL on a bad size. */
+kvt_manager* kvt_mgr_create(int64_t num_pages);
+void kvt_mgr_destroy(kvt_manager* m);
+int64_t kvt_mgr_free_pages(const kvt_manager* m);
+int64_t kvt_mgr_live_entries(const kvt_manager* m);
+
+/* Context events (KVT_ERR_INVALID_ARG on an unknown or terminated context,
+ * a bad message index, or an event the state does not allow: fork, one_off,
+ * replace, remove and terminate only between requests). */
+kvt_status kvt_mgr_spawn(kvt_manager* m, int64_t ctx);
+kvt_status kvt_mgr_fork(kvt_manager* m, int64_t parent, int64_t child);  /* child maps the parent's entries */
+kvt_status kvt_mgr_append(kvt_manager* m, int64_t ctx, int64_t tokens);   /* new message, Active (Temporary if one-off) */
+kvt_status kvt_mgr_one_off(kvt_manager* m, int64_t ctx);                  /* existing and later messages Temporary; Pinned stay */
+kvt_status kvt_mgr_pin(kvt_manager* m, int64_t ctx, int64_t msg_index);     /* not a Temporary message */
+kvt_status kvt_mgr_unpin(kvt_manager* m, int64_t ctx, int64_t msg_index);  /* -> Suspended; Active in a request, Temporary if one-off, Expired if terminated */
+kvt_status kvt_mgr_replace(kvt_manager* m, int64_t ctx, int64_t msg_index, int64_t tokens);
+kvt_status kvt_mgr_remove(kvt_manager* m, int64_t ctx, int64_t msg_index);
+    /* replace/remove: the versions of msg_index and of every later message expire; the
+       message (replace) and the later ones get fresh versions, Active (Temporary if one-off) */
+kvt_status kvt_mgr_terminate(kvt_manager* m, int64_t ctx);               /* ordinary messages expire; Pinned stay */
+
+/* A request's boundaries, in this order.
+ *   begin_request: the LLM call is issued; Suspended messages become Active
+ *     again.  Nothing is held yet: until its prefill starts, the request's
+ *     entries are Active-tier KV that admission may take (Algorithm 1's
+ *     Active step).
+ *   start_prefill: hits and misses are resolved against what is resident
+ *     now (report: hit_tokens, miss_tokens); the context's resident entries
+ *     are held until end_request, since the kernels read their pages.
+ *   prefill_done: every message without KV gets an entry, Active messages
+ *     become Suspended, and the new entries are admitted in message order
+ *     (report: admitted / bypassed / rejected / released).
+ *   end_request: the held entries become releasable; Active messages become
+ *     Suspended.  Allowed from any phase after begin (an abort). */
+kvt_status kvt_mgr_begin_request(kvt_manager* m, int64_t ctx);
+kvt_status kvt_mgr_start_prefill(kvt_manager* m, int64_t ctx, kvt_mgr_report* report);
+kvt_status kvt_mgr_prefill_done(kvt_manager* m, int64_t ctx, kvt_mgr_report* report);
+kvt_status kvt_mgr_end_request(kvt_manager* m, int64_t ctx);
+
+/* Queries (-1 for an unknown context or index).  message_pages: the page
+ * ids of the message's resident entry (up to cap written), their count, or
+ * -1 if it has none resident. */
+int32_t kvt_mgr_message_state(const kvt_manager* m, int64_t ctx, int64_t msg_index);
+int32_t kvt_mgr_entry_tier(const kvt_manager* m, int64_t ctx, int64_t msg_index);
+int64_t kvt_mgr_message_pages(const kvt_manager* m, int64_t ctx, int64_t msg_index, int32_t* pages, int64_t cap);
+
 /* Static English text for a status code (never NULL). */
 const char* kvt_status_str(kvt_status s);
 

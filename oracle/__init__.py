@@ -23,10 +23,14 @@ What it computes (the problem the paper frames and the definition it implies):
 * ``oracle_to_host`` / ``oracle_to_device`` -- whole pages moved between the
   HBM tier and a packed host buffer (tiered cache, §6; local GPU <-> CPU
   engine, §7): a bitwise copy in page-list order.
+* ``OracleManager`` -- the lifecycle states of message versions (§5.2), the
+  aggregate state of shared KV and Algorithm 1's state-prioritized admission
+  (§6.1), MRU eviction inside the Suspended tier (§6.2), written as a plain
+  list-scanning model.
 
-Every function here is pinned by ``tests/test_oracle_pins.py`` against brute
-force, closed forms, a library routine and invariants; none is
-"parity unpinned".
+Every function here is pinned by ``tests/test_oracle_pins.py`` (the manager
+by ``tests/test_manager.py``) against brute force, closed forms, a library
+routine, hand-worked traces and invariants; none is "parity unpinned".
 """
 from .attention import (  # noqa: F401
     storage_to_f64,
@@ -36,3 +40,4 @@ from .attention import (  # noqa: F401
     gather_logical,
 )
 from .blocks import oracle_to_device, oracle_to_host  # noqa: F401
+from .manager import OracleManager  # noqa: F401

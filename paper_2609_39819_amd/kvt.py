@@ -27,11 +27,18 @@ KVT_DTYPE_BF16 = 0
 KVT_DTYPE_F32 = 1
 BLOCK_SIZE = 16
 
+MGR_EXPORTED = ("kvt_mgr_append", "kvt_mgr_begin_request", "kvt_mgr_create", "kvt_mgr_destroy", "kvt_mgr_end_request",
+                "kvt_mgr_entry_tier", "kvt_mgr_fork", "kvt_mgr_free_pages", "kvt_mgr_live_entries",
+                "kvt_mgr_message_pages", "kvt_mgr_message_state", "kvt_mgr_one_off", "kvt_mgr_pin",
+                "kvt_mgr_prefill_done", "kvt_mgr_remove", "kvt_mgr_replace", "kvt_mgr_spawn", "kvt_mgr_start_prefill",
+                "kvt_mgr_terminate", "kvt_mgr_unpin")
 EXPORTED = ("kvt_append_kv", "kvt_cascade_extend_attention", "kvt_cascade_workspace_bytes", "kvt_copy_blocks",
             "kvt_decode_attention", "kvt_decode_workspace_bytes", "kvt_extend_attention",
-            "kvt_extend_workspace_bytes", "kvt_last_hip_error", "kvt_status_str")
+            "kvt_extend_workspace_bytes", "kvt_last_hip_error", "kvt_status_str") + MGR_EXPORTED
 KVT_COPY_TO_HOST = 0
 KVT_COPY_TO_DEVICE = 1
+KVT_PINNED, KVT_ACTIVE, KVT_SUSPENDED, KVT_EXPIRED, KVT_TEMPORARY = 0, 1, 2, 3, 4
+KVT_TIER_PINNED, KVT_TIER_ACTIVE, KVT_TIER_SUSPENDED, KVT_TIER_DISCARDED = 0, 1, 2, 3
 
 
 class KvtPool(ctypes.Structure):
@@ -43,6 +50,15 @@ class KvtSeqs(ctypes.Structure):
     _fields_ = [("num_seqs", ctypes.c_int32), ("prefix_len", ctypes.POINTER(ctypes.c_int32)),
                 ("suffix_len", ctypes.POINTER(ctypes.c_int32)), ("block_table", ctypes.c_void_p),
                 ("block_table_host", ctypes.POINTER(ctypes.c_int32)), ("max_blocks", ctypes.c_int32)]
+
+
+class KvtMgrReport(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in ("admitted_entries", "admitted_pages", "bypassed_entries",
+                                               "rejected_entries", "released_entries", "released_pages",
+                                               "hit_tokens", "miss_tokens")]
+
+    def as_dict(self) -> dict:
+        return {n: int(getattr(self, n)) for n, _ in self._fields_}
 
 
 class KvtError(RuntimeError):
@@ -84,6 +100,22 @@ def lib():
         L.kvt_decode_attention.restype = ctypes.c_int
         L.kvt_decode_workspace_bytes.argtypes = L.kvt_extend_workspace_bytes.argtypes
         L.kvt_decode_workspace_bytes.restype = ctypes.c_size_t
+        M, I64, I32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32
+        L.kvt_mgr_create.argtypes, L.kvt_mgr_create.restype = [I64], M
+        L.kvt_mgr_destroy.argtypes, L.kvt_mgr_destroy.restype = [M], None
+        for name in ("kvt_mgr_free_pages", "kvt_mgr_live_entries"):
+            getattr(L, name).argtypes, getattr(L, name).restype = [M], I64
+        for name, args in (("kvt_mgr_spawn", [I64]), ("kvt_mgr_fork", [I64, I64]), ("kvt_mgr_append", [I64, I64]),
+                           ("kvt_mgr_one_off", [I64]), ("kvt_mgr_pin", [I64, I64]), ("kvt_mgr_unpin", [I64, I64]),
+                           ("kvt_mgr_replace", [I64, I64, I64]), ("kvt_mgr_remove", [I64, I64]),
+                           ("kvt_mgr_terminate", [I64]), ("kvt_mgr_begin_request", [I64]),
+                           ("kvt_mgr_start_prefill", [I64, P(KvtMgrReport)]),
+                           ("kvt_mgr_prefill_done", [I64, P(KvtMgrReport)]), ("kvt_mgr_end_request", [I64])):
+            getattr(L, name).argtypes, getattr(L, name).restype = [M] + args, ctypes.c_int
+        for name in ("kvt_mgr_message_state", "kvt_mgr_entry_tier"):
+            getattr(L, name).argtypes, getattr(L, name).restype = [M, I64, I64], I32
+        L.kvt_mgr_message_pages.argtypes = [M, I64, I64, P(I32), I64]
+        L.kvt_mgr_message_pages.restype = I64
         L.kvt_status_str.argtypes = [ctypes.c_int]
         L.kvt_status_str.restype = ctypes.c_char_p
         L.kvt_last_hip_error.argtypes = []
@@ -292,3 +324,81 @@ def _attention(entry: str, ws_entry: str, q, k_pool, v_pool, block_table, prefix
     if st != KVT_OK:
         raise KvtError(st, entry)
     return (out, lse) if want_lse else out
+
+
+# ---------------------------------------------------------------------------
+# host block manager
+# ---------------------------------------------------------------------------
+
+class Manager:
+    """The library's host block manager over ``num_pages`` KV pages.
+
+    Each method is one ``kvt_mgr_*`` call; a non-OK status raises
+    ``KvtError``.  Request-boundary calls return the report as a dict."""
+
+    def __init__(self, num_pages: int):
+        self._h = lib().kvt_mgr_create(int(num_pages))
+        if not self._h:
+            raise ValueError(f"kvt_mgr_create: bad page count {num_pages}")
+
+    def close(self):
+        if self._h:
+            lib().kvt_mgr_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def _call(self, name: str, *args):
+        st = getattr(lib(), name)(self._h, *[int(a) for a in args])
+        if st != KVT_OK:
+            raise KvtError(st, name)
+
+    def _report(self, name: str, ctx: int) -> dict:
+        rep = KvtMgrReport()
+        st = getattr(lib(), name)(self._h, int(ctx), ctypes.byref(rep))
+        if st != KVT_OK:
+            raise KvtError(st, name)
+        return rep.as_dict()
+
+    def spawn(self, ctx): self._call("kvt_mgr_spawn", ctx)
+    def fork(self, parent, child): self._call("kvt_mgr_fork", parent, child)
+    def append(self, ctx, tokens): self._call("kvt_mgr_append", ctx, tokens)
+    def one_off(self, ctx): self._call("kvt_mgr_one_off", ctx)
+    def pin(self, ctx, i): self._call("kvt_mgr_pin", ctx, i)
+    def unpin(self, ctx, i): self._call("kvt_mgr_unpin", ctx, i)
+    def replace(self, ctx, i, tokens): self._call("kvt_mgr_replace", ctx, i, tokens)
+    def remove(self, ctx, i): self._call("kvt_mgr_remove", ctx, i)
+    def terminate(self, ctx): self._call("kvt_mgr_terminate", ctx)
+    def begin_request(self, ctx): self._call("kvt_mgr_begin_request", ctx)
+    def end_request(self, ctx): self._call("kvt_mgr_end_request", ctx)
+
+    def start_prefill(self, ctx) -> dict:
+        return self._report("kvt_mgr_start_prefill", ctx)
+
+    def prefill_done(self, ctx) -> dict:
+        return self._report("kvt_mgr_prefill_done", ctx)
+
+    def free_pages(self) -> int:
+        return int(lib().kvt_mgr_free_pages(self._h))
+
+    def live_entries(self) -> int:
+        return int(lib().kvt_mgr_live_entries(self._h))
+
+    def message_state(self, ctx, i) -> int:
+        return int(lib().kvt_mgr_message_state(self._h, int(ctx), int(i)))
+
+    def entry_tier(self, ctx, i) -> Optional[int]:
+        t = int(lib().kvt_mgr_entry_tier(self._h, int(ctx), int(i)))
+        return None if t < 0 else t
+
+    def message_pages(self, ctx, i) -> Optional[list]:
+        n = int(lib().kvt_mgr_message_pages(self._h, int(ctx), int(i), None, 0))
+        if n < 0:
+            return None
+        buf = (ctypes.c_int32 * max(n, 1))()
+        lib().kvt_mgr_message_pages(self._h, int(ctx), int(i), buf, n)
+        return list(buf[:n])

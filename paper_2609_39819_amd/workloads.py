@@ -415,3 +415,107 @@ def stage_on_device(w: Workload, device="cuda", num_blocks: Optional[int] = None
         v_new=np_to_torch(w.v_new, w.dtype, device),
         block_table=torch.from_numpy(w.block_table).to(device),
     )
+
+
+# --------------------------------------------------------------------------
+# event trace for the host block manager
+# --------------------------------------------------------------------------
+
+def agent_events(seed: int = 9, agents: int = 256, concurrency: int = 32, calls=(8, 40),
+                 system_tokens=(512, 4096), tool_tokens=(64, 4096), tool_wait=(16, 128), fork_prob: float = 0.1,
+                 one_off_prob: float = 0.08, edit_prob: float = 0.03, pin_prob: float = 0.25):
+    """A seeded stream of block-manager calls from interleaved ReAct agents.
+
+    Each agent spawns, appends a system prompt (pinned for a share of agents)
+    and a task, then runs U[calls] LLM calls -- issue, start of prefill, end
+    of prefill, end of request -- each followed by a tool output of
+    U[tool_tokens] tokens appended as a new message (paper §2.2, §5.2).  At
+    a call boundary an agent may fork a sub-agent that runs a few calls over
+    the shared prefix and terminates, or edit an earlier message (replace);
+    a share of agents are one-off.  At most ``concurrency`` agents (plus
+    their sub-agents) run at once, their next events interleaved at random;
+    while its tool runs, an agent sits out U[tool_wait] events of the others
+    (so few requests are in flight at once, as in a ReAct workload where
+    tools and LLM calls alternate); an agent unpins its system prompt and
+    terminates when done.
+
+    Yields ``(op, args)`` with the method names of the manager; every call
+    is valid for the state the earlier calls produce.  Token counts only --
+    no attention arithmetic.
+    """
+    rng = np.random.default_rng(seed)
+    next_id = [0]
+
+    def new_id():
+        next_id[0] += 1
+        return next_id[0] - 1
+
+    def call(c):
+        yield "begin_request", (c,)
+        yield "start_prefill", (c,)
+        yield "prefill_done", (c,)
+        yield "end_request", (c,)
+        yield "wait", int(rng.integers(tool_wait[0], tool_wait[1], endpoint=True))
+
+    def sub_agent(c, n_calls, n_msgs):
+        for _ in range(n_calls):
+            yield from call(c)
+            yield "append", (c, int(rng.integers(tool_tokens[0], tool_tokens[1], endpoint=True)))
+            n_msgs += 1
+        yield "terminate", (c,)
+
+    def agent(c):
+        yield "spawn", (c,)
+        yield "append", (c, int(rng.integers(system_tokens[0], system_tokens[1], endpoint=True)))
+        pinned = rng.random() < pin_prob
+        if pinned:
+            yield "pin", (c, 0)
+        yield "append", (c, int(rng.integers(32, 512, endpoint=True)))
+        n_msgs = 2
+        if rng.random() < one_off_prob:
+            yield "one_off", (c,)
+            yield from call(c)
+            yield "terminate", (c,)
+            if pinned:
+                yield "unpin", (c, 0)
+            return
+        for _ in range(int(rng.integers(calls[0], calls[1], endpoint=True))):
+            yield from call(c)
+            yield "append", (c, int(rng.integers(tool_tokens[0], tool_tokens[1], endpoint=True)))
+            n_msgs += 1
+            u = rng.random()
+            if u < fork_prob:
+                k = new_id()
+                yield "fork", (c, k)
+                yield ("start", sub_agent(k, int(rng.integers(2, 6, endpoint=True)), n_msgs))
+            elif u < fork_prob + edit_prob and n_msgs > 3:
+                yield "replace", (c, int(rng.integers(2, n_msgs)), int(rng.integers(tool_tokens[0], tool_tokens[1])))
+        yield "terminate", (c,)
+        if pinned:
+            yield "unpin", (c, 0)
+
+    running, wake, started, t = [], [], 0, 0      # programs, the event count each may resume at
+    while running or started < agents:
+        while started < agents and len(running) < concurrency:
+            running.append(agent(new_id()))
+            wake.append(t)
+            started += 1
+        ready = [i for i in range(len(running)) if wake[i] <= t]
+        if not ready:
+            t = min(wake)
+            continue
+        i = ready[int(rng.integers(0, len(ready)))]
+        try:
+            ev = next(running[i])
+        except StopIteration:
+            running.pop(i)
+            wake.pop(i)
+            continue
+        if ev[0] == "start":
+            running.append(ev[1])
+            wake.append(t)
+        elif ev[0] == "wait":
+            wake[i] = t + ev[1]
+        else:
+            t += 1
+            yield ev
