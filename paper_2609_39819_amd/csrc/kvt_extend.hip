@@ -157,8 +157,28 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
     const int slot = min(keyrow[i] & (kBlock - 1), last);
     return ((((int64_t)id * hkv + g) << 4) + slot) * D + chunk_off[i];
   };
+  // in a tile whose 64 positions all lie inside the sequence, a lane's byte
+  // offset within its page run is a constant over the wave-uniform page base
+  uint32_t lane_byte[NREG];
+#pragma unroll
+  for (int i = 0; i < NREG; ++i) lane_byte[i] = (uint32_t)(((keyrow[i] & (kBlock - 1)) * D + chunk_off[i]) * 2);
   u32x4 stK[NREG], stV[NREG];   // register staging (fp32 storage only)
   auto issue = [&](int jn, const uint32_t (&ids)[NREG], const Slot<D>& dst) __attribute__((always_inline)) {
+    if constexpr (kDirect) {
+      if ((jn + 1) * KT <= L) {
+#pragma unroll
+        for (int i = 0; i < NREG; ++i) {
+          const int64_t base = (((int64_t)ids[i] * hkv + g) << 4) * D;
+          const char* ks = reinterpret_cast<const char*>(kpool + base) + lane_byte[i];
+          const char* vs = reinterpret_cast<const char*>(vpool + base) + lane_byte[i];
+          lds_bf16* kd = (lds_bf16*)dst.k.e + lds_off[i];
+          lds_bf16* vd = (lds_bf16*)dst.v.e + lds_off[i];
+          __builtin_amdgcn_global_load_lds((const void*)ks, (__attribute__((address_space(3))) void*)kd, 16, 0, 0);
+          __builtin_amdgcn_global_load_lds((const void*)vs, (__attribute__((address_space(3))) void*)vd, 16, 0, 0);
+        }
+        return;
+      }
+    }
 #pragma unroll
     for (int i = 0; i < NREG; ++i) {
       const int64_t off = src_off(jn, i, ids[i]);
@@ -231,26 +251,30 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
   // tile's first query), row max, and the reference-max update.  The
   // reference only moves when a tile max passes it by more than the slack;
   // O and l are then rescaled (rare after the first tiles).
+  // Element e of half h of a lane's scores is key j*KT + 4*hh + koff(h, e)
+  // with koff(h, e) = 32h + 8(e/4) + e%4 in 0..59: the masks compare that
+  // constant against one per-lane threshold, so no key index is formed.
   auto settle = [&](int j, f32x16 (&s)[NB][2]) __attribute__((always_inline)) {
     if (j * KT + KT - 1 > lim_min) {
 #pragma unroll
-      for (int b = 0; b < NB; ++b)
+      for (int b = 0; b < NB; ++b) {
+        const int thr = lim[b] - j * KT - 4 * hh;        // keys past lim: koff > thr
 #pragma unroll
         for (int half = 0; half < 2; ++half)
 #pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int kabs = j * KT + half * 32 + 8 * (e >> 2) + 4 * hh + (e & 3);
-            if (kabs > lim[b]) s[b][half][e] = -INFINITY;
-          }
+          for (int e = 0; e < 16; ++e)
+            if (half * 32 + 8 * (e >> 2) + (e & 3) > thr) s[b][half][e] = -INFINITY;
+      }
     }
     if (j * KT < a.kbeg) {   // first tile of a range that starts inside it
+      const int thr = a.kbeg - j * KT - 4 * hh;          // keys before kbeg: koff < thr
 #pragma unroll
       for (int b = 0; b < NB; ++b)
 #pragma unroll
         for (int half = 0; half < 2; ++half)
 #pragma unroll
           for (int e = 0; e < 16; ++e)
-            if (j * KT + half * 32 + 8 * (e >> 2) + 4 * hh + (e & 3) < a.kbeg) s[b][half][e] = -INFINITY;
+            if (half * 32 + 8 * (e >> 2) + (e & 3) < thr) s[b][half][e] = -INFINITY;
     }
     float alpha[NB];
     bool moved = false;
