@@ -236,16 +236,29 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
     const __bf16* ks = tl.k.e;
 #pragma unroll
     for (int b = 0; b < NB; ++b) s[b][0] = s[b][1] = (f32x16){};
+    bf16x8 kf[KSTEPS][2];
 #pragma unroll
     for (int kk = 0; kk < KSTEPS; ++kk) {
-      const bf16x8 k0 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(ks + koff[kk]));
-      const bf16x8 k1 = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(ks + koff[kk] + 32 * D));
+      kf[kk][0] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(ks + koff[kk]));
+      kf[kk][1] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(ks + koff[kk] + 32 * D));
+    }
+#pragma unroll
+    for (int kk = 0; kk < KSTEPS; ++kk) {
 #pragma unroll
       for (int b = 0; b < NB; ++b) {
-        s[b][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qreg[b][kk], s[b][0], 0, 0, 0);
-        s[b][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qreg[b][kk], s[b][1], 0, 0, 0);
+        s[b][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk][0], qreg[b][kk], s[b][0], 0, 0, 0);
+        s[b][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[kk][1], qreg[b][kk], s[b][1], 0, 0, 0);
       }
     }
+    // K fragments read ahead of the products that use them: two steps'
+    // worth first, then each pair of products followed by the next pair of reads
+    __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+    for (int kk = 0; kk < KSTEPS - 2; ++kk) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2 * NB, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 4 * NB, 0);
   };
   // ---- between tiles: causal mask of tile j (only tiles reaching past the
   // tile's first query), row max, and the reference-max update.  The
