@@ -297,8 +297,9 @@ kvt_status kvt_mgr_prefill_done(kvt_manager* m, int64_t ctx, kvt_mgr_report* rep
 kvt_status kvt_mgr_end_request(kvt_manager* m, int64_t ctx);
 
 /* Queries (-1 for an unknown context or index).  message_pages: the page
- * ids of the message's resident entry (up to cap written), their count, or
- * -1 if it has none resident. */
+ * ids of the message's resident entry (up to cap written; pages may be NULL
+ * to ask for the count), their count, or -1 if it has none resident.
+ * Token counts (append, replace) are 1 .. 2^40. */
 int32_t kvt_mgr_message_state(const kvt_manager* m, int64_t ctx, int64_t msg_index);
 int32_t kvt_mgr_entry_tier(const kvt_manager* m, int64_t ctx, int64_t msg_index);
 int64_t kvt_mgr_message_pages(const kvt_manager* m, int64_t ctx, int64_t msg_index, int32_t* pages, int64_t cap);

@@ -33,6 +33,7 @@ started holds nothing, and its reactivated KV is the Active tier.
 from __future__ import annotations
 
 PINNED, ACTIVE, SUSPENDED, EXPIRED, TEMPORARY = 0, 1, 2, 3, 4
+MAX_TOKENS = 1 << 40                # per message (the library's bound)
 T_PINNED, T_ACTIVE, T_SUSPENDED, T_DISCARDED = 0, 1, 2, 3
 
 
@@ -171,8 +172,8 @@ class OracleManager:
 
     def append(self, c, tokens):
         self._tick()
-        if tokens < 1:
-            raise ValueError("empty message")
+        if not 1 <= tokens <= MAX_TOKENS:
+            raise ValueError("bad message size")
         ctx = self._ctx(c)
         ctx.msgs.append(self._fresh(ctx, tokens))
 
@@ -216,7 +217,7 @@ class OracleManager:
     def replace(self, c, i, tokens):
         self._tick()
         ctx = self._ctx(c)
-        if ctx.phase != IDLE or tokens < 1 or not 0 <= i < len(ctx.msgs):
+        if ctx.phase != IDLE or not 1 <= tokens <= MAX_TOKENS or not 0 <= i < len(ctx.msgs):
             raise ValueError("bad replace")
         self._expire_from(ctx, i)
         ctx.msgs[i].tokens = tokens

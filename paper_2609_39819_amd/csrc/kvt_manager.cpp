@@ -45,6 +45,7 @@
 namespace {
 
 enum State : int { kPinned = 0, kActive = 1, kSuspended = 2, kExpired = 3, kTemporary = 4 };
+constexpr int64_t kMaxTokens = int64_t{1} << 40;   // per message; keeps page counts far from overflow
 constexpr int kStates = 5;
 // aggregate tiers, strongest first; Expired and Temporary both map to Discarded
 enum Tier : int { kTierPinned = 0, kTierActive = 1, kTierSuspended = 2, kTierDiscarded = 3 };
@@ -84,10 +85,11 @@ struct Context {
 class PageSet {
  public:
   void reset(int64_t n) {
-    words_.assign((size_t)((n + 63) / 64), 0);
-    summary_.assign((words_.size() + 63) / 64, 0);
-    count_ = 0;
-    for (int64_t p = 0; p < n; ++p) give((int32_t)p);
+    words_.assign((size_t)((n + 63) / 64), ~0ull);
+    if (n % 64) words_.back() = (1ull << (n % 64)) - 1;
+    summary_.assign((words_.size() + 63) / 64, ~0ull);
+    if (words_.size() % 64) summary_.back() = (1ull << (words_.size() % 64)) - 1;
+    count_ = n;
   }
   int64_t size() const { return count_; }
   void give(int32_t p) {
@@ -284,7 +286,7 @@ kvt_status kvt_mgr_fork(kvt_manager* m, int64_t parent, int64_t child) {
 kvt_status kvt_mgr_append(kvt_manager* m, int64_t ctx, int64_t tokens) {
   if (m != nullptr) ++m->event;
   Context* c = find_ctx(m, ctx);
-  if (c == nullptr || c->terminated || tokens < 1) return KVT_ERR_INVALID_ARG;
+  if (c == nullptr || c->terminated || tokens < 1 || tokens > kMaxTokens) return KVT_ERR_INVALID_ARG;
   Message msg;
   msg.state = c->one_off ? kTemporary : kActive;
   msg.tokens = tokens;
@@ -326,7 +328,7 @@ kvt_status kvt_mgr_unpin(kvt_manager* m, int64_t ctx, int64_t msg_index) {
 kvt_status kvt_mgr_replace(kvt_manager* m, int64_t ctx, int64_t msg_index, int64_t tokens) {
   if (m != nullptr) ++m->event;
   Context* c = find_ctx(m, ctx);
-  if (c == nullptr || c->terminated || c->phase != kIdle || tokens < 1 || msg_index < 0 ||
+  if (c == nullptr || c->terminated || c->phase != kIdle || tokens < 1 || tokens > kMaxTokens || msg_index < 0 ||
       msg_index >= (int64_t)c->msgs.size())
     return KVT_ERR_INVALID_ARG;
   expire_from(m, *c, (size_t)msg_index);
@@ -440,7 +442,8 @@ int64_t kvt_mgr_message_pages(const kvt_manager* m, int64_t ctx, int64_t msg_ind
   const Entry& e = m->entries.at(msg.entry);
   if (!e.resident) return -1;
   const int64_t n = (int64_t)e.page_ids.size();
-  for (int64_t i = 0; i < n && i < cap; ++i) pages[i] = e.page_ids[i];
+  if (pages != nullptr)
+    for (int64_t i = 0; i < n && i < cap; ++i) pages[i] = e.page_ids[i];
   return n;
 }
 

@@ -277,6 +277,54 @@ def test_pin_event_rules(make):
     assert m.message_state(1, 0) == EXPIRED and m.entry_tier(1, 0) == T_DISCARDED
 
 
+@pytest.mark.parametrize("pages", [0, 1, 63, 64, 65, 4095, 4096, 4097, 70000])
+def test_pool_sizes_across_bitmap_words(pages):
+    """Fill the pool, free a scattered part of it and refill: the library's
+    two-level bitmap hands out the same lowest ids as the oracle's set."""
+    o, lib = OracleManager(pages), kvt.Manager(pages)
+    assert lib.free_pages() == pages
+    rng = np.random.default_rng(pages)
+    sizes = []
+    left = pages
+    while left > 0:
+        t = int(rng.integers(1, 40 * 16))
+        sizes.append(t)
+        left -= (t + 15) // 16
+    for m in (o, lib):
+        for c, t in enumerate(sizes):
+            new_ctx(m, c, t)
+            serve(m, c)
+        for c in range(0, len(sizes), 3):
+            m.terminate(c)
+        new_ctx(m, 10**6, max(1, pages // 2) * 16)
+        serve(m, 10**6)
+    for c in list(range(len(sizes))) + [10**6]:
+        assert o.message_pages(c, 0) == lib.message_pages(c, 0), c
+    assert o.free_pages() == lib.free_pages()
+
+
+def test_manager_bounds():
+    lib = kvt.Manager(4)
+    lib.spawn(1)
+    for bad in (0, -5, (1 << 40) + 1):
+        with pytest.raises(kvt.KvtError):
+            lib.append(1, bad)
+    lib.append(1, 1 << 40)                               # the largest message is accepted ...
+    lib.begin_request(1)
+    lib.start_prefill(1)
+    assert lib.prefill_done(1)["rejected_entries"] == 1  # ... and does not fit
+    lib.append(1, 20)
+    lib.end_request(1)
+    serve(lib, 1)
+    assert kvt.lib().kvt_mgr_message_pages(lib._h, 1, 1, None, 5) == 2   # NULL buffer: count only
+    assert lib.message_pages(1, 1) == [0, 1]
+    assert kvt.Manager(0).free_pages() == 0
+    with pytest.raises(ValueError):
+        kvt.Manager(-1)
+    with pytest.raises(ValueError):
+        kvt.Manager(1 << 31)
+
+
 # ---------------------------------------------------------------------------
 # library vs oracle on seeded random event streams
 # ---------------------------------------------------------------------------
