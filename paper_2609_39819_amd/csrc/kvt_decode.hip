@@ -5,9 +5,12 @@
 // sequence contributes G = Hq/Hkv query rows per kv-head, and the cost is
 // streaming the sequence's K/V once from HBM.  Work decomposition:
 //   * one workgroup per (sequence, kv-head, key split), 4 waves;
-//   * wave w takes the split's 32-key tiles w, w+4, w+8, ... through its own
-//     two-slot LDS ring: the ring is private to the wave, so the loop has no
-//     barrier -- a wave waits only for its own page gathers;
+//   * wave w takes the split's 32-key tiles w, w+4, w+8, ...: each tile is
+//     loaded into registers two tiles ahead of its use and stored into the
+//     wave's own LDS slot just before it is needed; the slot is private to
+//     the wave, so the loop has no barrier (plain loads into registers
+//     stream faster from HBM than LDS-DMA gathers, and keep two tiles per
+//     wave in flight);
 //   * per tile: S^T = K Q^T and O^T += V^T P^T on one 32-row MFMA block
 //     (v_mfma_f32_32x32x16_bf16; rows >= G repeat row G-1 and are dropped),
 //     with the online softmax of the extend kernel (lazy reference max);
@@ -41,12 +44,8 @@ __global__ __launch_bounds__(kWaves * 64) void decode_kernel(const ExtendArgs a)
   constexpr int NLD = kTK * ROWB / 1024;         // 1 KiB loads per tensor per tile
   constexpr int KSTEPS = D / 16;
   constexpr int DT = D / 32;
-  constexpr bool kDirect = sizeof(T) == 2;
   constexpr float kRescaleSlack = 8.0f;
-  // slot 0 and slot 1 of every wave's ring are distinct objects, so the
-  // compiler can tell the gather into one slot from the reads of the other
-  __shared__ __attribute__((aligned(1024))) DecSlot<D> ring0[kWaves];
-  __shared__ __attribute__((aligned(1024))) DecSlot<D> ring1[kWaves];
+  __shared__ __attribute__((aligned(1024))) DecSlot<D> ring0[kWaves];   // one slot per wave
   __shared__ float ml[kWaves][32][2];            // per wave and row: m (log2 units), l
 
   const int tid = threadIdx.x;
@@ -104,33 +103,27 @@ __global__ __launch_bounds__(kWaves * 64) void decode_kernel(const ExtendArgs a)
       ids[p] = __builtin_amdgcn_readfirstlane(raw > nb_max ? nb_max : raw);
     }
   };
-  u32x4 stK[NLD], stV[NLD];   // register staging (fp32 storage only)
+  // one tile's K and V as this lane's 16-byte pieces, in registers
+  struct Stage {
+    u32x4 k[NLD], v[NLD];
+  };
   // positions past the end read the last real position (finite; weight 0)
-  auto issue = [&](int j, const uint32_t (&ids)[2], DecSlot<D>& dst) __attribute__((always_inline)) {
+  auto load_tile = [&](int j, const uint32_t (&ids)[2], Stage& st) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
       const int p = (RPR * i) / kBlock;
       const int page = min(j * 2 + p, nblk - 1);
       const int slot = min((RPR * i + lane / CHUNKS) & (kBlock - 1), L - 1 - page * kBlock);
       const int64_t off = ((((int64_t)ids[p] * hkv + g) << 4) + slot) * D + chunk_off[i];
-      if constexpr (kDirect) {
-        __builtin_amdgcn_global_load_lds((const void*)(kpool + off),
-                                         (__attribute__((address_space(3))) void*)((lds_bf16*)dst.k + i * 512), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds((const void*)(vpool + off),
-                                         (__attribute__((address_space(3))) void*)((lds_bf16*)dst.v + i * 512), 16, 0, 0);
-      } else {
-        stK[i] = load8(kpool + off);
-        stV[i] = load8(vpool + off);
-      }
+      st.k[i] = load8(kpool + off);
+      st.v[i] = load8(vpool + off);
     }
   };
-  auto stash = [&](DecSlot<D>& dst) __attribute__((always_inline)) {
-    if constexpr (!kDirect) {
+  auto stash = [&](const Stage& st, DecSlot<D>& dst) __attribute__((always_inline)) {
 #pragma unroll
-      for (int i = 0; i < NLD; ++i) {
-        *reinterpret_cast<u32x4*>(dst.k + i * 512 + lane * 8) = stK[i];
-        *reinterpret_cast<u32x4*>(dst.v + i * 512 + lane * 8) = stV[i];
-      }
+    for (int i = 0; i < NLD; ++i) {
+      *reinterpret_cast<u32x4*>(dst.k + i * 512 + lane * 8) = st.k[i];
+      *reinterpret_cast<u32x4*>(dst.v + i * 512 + lane * 8) = st.v[i];
     }
   };
 
@@ -207,35 +200,37 @@ __global__ __launch_bounds__(kWaves * 64) void decode_kernel(const ExtendArgs a)
       }
   };
 
-  // ---- this wave's tiles j0 + wave + kWaves*i, double-buffered.  Step i
-  // starts the gather of tile i+1 into the other slot, waits for its own
-  // loads of tile i (the newer ones may stay in flight) and computes tile i.
-  constexpr int LPT = 2 * NLD;                   // gather loads per tile
+  // ---- this wave's tiles j0 + wave + kWaves*i.  Tile i+1 is in registers
+  // (possibly still in flight) when step i starts; step i starts loading tile
+  // i+2 into the registers tile i left, computes tile i from the slot, then
+  // stores tile i+1 into the slot (the wave's LDS operations run in order,
+  // so the stores follow the reads of tile i).
   DecSlot<D>& s0 = ring0[wave];
-  DecSlot<D>& s1 = ring1[wave];
+  auto jt = [&](int i) { return j0 + wave + kWaves * i; };
+  Stage sa, sb;
   uint32_t ids[2];
   if (nt > 0) {
-    page_ids(j0 + wave, ids);
-    issue(j0 + wave, ids, s0);
-    stash(s0);
-    page_ids(j0 + wave + kWaves, ids);
-  }
-  auto step = [&](int i, DecSlot<D>& cur, DecSlot<D>& nxt) __attribute__((always_inline)) {
-    const int j = j0 + wave + kWaves * i;
-    if (i + 1 < nt) {
-      issue(j + kWaves, ids, nxt);
-      stash(nxt);
-      page_ids(j + 2 * kWaves, ids);
-      __builtin_amdgcn_s_waitcnt(vmcnt_imm(kDirect ? LPT : 0));   // tile i landed
-    } else {
-      __builtin_amdgcn_s_waitcnt(vmcnt_imm(0));
+    page_ids(jt(0), ids);
+    load_tile(jt(0), ids, sa);
+    if (nt > 1) {
+      page_ids(jt(1), ids);
+      load_tile(jt(1), ids, sb);
     }
-    tile(cur, j * kTK);
+    page_ids(jt(2), ids);
+    stash(sa, s0);
+  }
+  auto step = [&](int i, Stage& nxt, Stage& fill) __attribute__((always_inline)) {
+    if (i + 2 < nt) {
+      load_tile(jt(i + 2), ids, fill);
+      page_ids(jt(i + 3), ids);
+    }
+    tile(s0, jt(i) * kTK);
+    if (i + 1 < nt) stash(nxt, s0);
   };
   for (int i = 0; i < nt; i += 2) {
-    step(i, s0, s1);
+    step(i, sb, sa);
     if (i + 1 >= nt) break;
-    step(i + 1, s1, s0);
+    step(i + 1, sa, sb);
   }
 
   // ---- merge the four waves.  Each wave parks its O (fp32, [row][D]) in
