@@ -296,6 +296,23 @@ kvt_status kvt_mgr_start_prefill(kvt_manager* m, int64_t ctx, kvt_mgr_report* re
 kvt_status kvt_mgr_prefill_done(kvt_manager* m, int64_t ctx, kvt_mgr_report* report);
 kvt_status kvt_mgr_end_request(kvt_manager* m, int64_t ctx);
 
+/* Trace replay, for callers that drive the manager from a recorded event
+ * trace (the paper evaluates on replayed agent traces, section 8.1): n
+ * events, each four int64 {op, a, b, c}, op one of KVT_MGR_OP_* and a, b, c
+ * the arguments of that call in order (context, then index / child /
+ * tokens, then tokens; unused ones ignored).  Each event runs exactly as the
+ * matching call; a failing event is skipped.  The reports of start_prefill
+ * and prefill_done are summed into totals (NULL: not reported).  Returns
+ * the number of events that returned KVT_OK, or -1 for a NULL manager, a
+ * NULL event array with n > 0, or n < 0. */
+enum {
+  KVT_MGR_OP_SPAWN = 0, KVT_MGR_OP_FORK = 1, KVT_MGR_OP_APPEND = 2, KVT_MGR_OP_ONE_OFF = 3, KVT_MGR_OP_PIN = 4,
+  KVT_MGR_OP_UNPIN = 5, KVT_MGR_OP_REPLACE = 6, KVT_MGR_OP_REMOVE = 7, KVT_MGR_OP_TERMINATE = 8,
+  KVT_MGR_OP_BEGIN_REQUEST = 9, KVT_MGR_OP_START_PREFILL = 10, KVT_MGR_OP_PREFILL_DONE = 11,
+  KVT_MGR_OP_END_REQUEST = 12
+};
+int64_t kvt_mgr_replay(kvt_manager* m, const int64_t* events, int64_t n, kvt_mgr_report* totals);
+
 /* Queries (-1 for an unknown context or index).  message_pages: the page
  * ids of the message's resident entry (up to cap written; pages may be NULL
  * to ask for the count), their count, or -1 if it has none resident.

@@ -90,17 +90,20 @@ class PageSet {
     summary_.assign((words_.size() + 63) / 64, ~0ull);
     if (words_.size() % 64) summary_.back() = (1ull << (words_.size() % 64)) - 1;
     count_ = n;
+    lo_ = 0;
   }
   int64_t size() const { return count_; }
   void give(int32_t p) {
     words_[(size_t)p >> 6] |= 1ull << (p & 63);
     summary_[(size_t)p >> 12] |= 1ull << ((p >> 6) & 63);
+    lo_ = std::min(lo_, (size_t)p >> 12);
     ++count_;
   }
   // the lowest free page, taken; the caller checks size() first
   int32_t take_lowest() {
-    size_t s = 0;
+    size_t s = lo_;
     while (summary_[s] == 0) ++s;
+    lo_ = s;
     const size_t w = s * 64 + (size_t)__builtin_ctzll(summary_[s]);
     const int b = __builtin_ctzll(words_[w]);
     words_[w] &= words_[w] - 1;
@@ -112,6 +115,7 @@ class PageSet {
  private:
   std::vector<uint64_t> words_, summary_;
   int64_t count_ = 0;
+  size_t lo_ = 0;   // no summary word below it has a free page
 };
 
 }  // namespace
@@ -426,6 +430,48 @@ kvt_status kvt_mgr_end_request(kvt_manager* m, int64_t ctx) {
   for (Message& msg : c->msgs)               // ordinary messages idle again
     if (msg.state == kActive) m->set_state(msg, kSuspended);
   return KVT_OK;
+}
+
+int64_t kvt_mgr_replay(kvt_manager* m, const int64_t* events, int64_t n, kvt_mgr_report* totals) {
+  if (m == nullptr || n < 0 || (n > 0 && events == nullptr)) return -1;
+  if (totals != nullptr) *totals = kvt_mgr_report{};
+  int64_t ok = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    const int64_t* e = events + 4 * i;
+    const int64_t a = e[1], b = e[2], c = e[3];
+    kvt_mgr_report rep{};
+    bool with_report = false;
+    kvt_status st = KVT_ERR_INVALID_ARG;
+    switch (e[0]) {
+      case KVT_MGR_OP_SPAWN: st = kvt_mgr_spawn(m, a); break;
+      case KVT_MGR_OP_FORK: st = kvt_mgr_fork(m, a, b); break;
+      case KVT_MGR_OP_APPEND: st = kvt_mgr_append(m, a, b); break;
+      case KVT_MGR_OP_ONE_OFF: st = kvt_mgr_one_off(m, a); break;
+      case KVT_MGR_OP_PIN: st = kvt_mgr_pin(m, a, b); break;
+      case KVT_MGR_OP_UNPIN: st = kvt_mgr_unpin(m, a, b); break;
+      case KVT_MGR_OP_REPLACE: st = kvt_mgr_replace(m, a, b, c); break;
+      case KVT_MGR_OP_REMOVE: st = kvt_mgr_remove(m, a, b); break;
+      case KVT_MGR_OP_TERMINATE: st = kvt_mgr_terminate(m, a); break;
+      case KVT_MGR_OP_BEGIN_REQUEST: st = kvt_mgr_begin_request(m, a); break;
+      case KVT_MGR_OP_START_PREFILL: st = kvt_mgr_start_prefill(m, a, &rep); with_report = true; break;
+      case KVT_MGR_OP_PREFILL_DONE: st = kvt_mgr_prefill_done(m, a, &rep); with_report = true; break;
+      case KVT_MGR_OP_END_REQUEST: st = kvt_mgr_end_request(m, a); break;
+      default: break;
+    }
+    if (st != KVT_OK) continue;
+    ++ok;
+    if (with_report && totals != nullptr) {
+      totals->admitted_entries += rep.admitted_entries;
+      totals->admitted_pages += rep.admitted_pages;
+      totals->bypassed_entries += rep.bypassed_entries;
+      totals->rejected_entries += rep.rejected_entries;
+      totals->released_entries += rep.released_entries;
+      totals->released_pages += rep.released_pages;
+      totals->hit_tokens += rep.hit_tokens;
+      totals->miss_tokens += rep.miss_tokens;
+    }
+  }
+  return ok;
 }
 
 int32_t kvt_mgr_message_state(const kvt_manager* m, int64_t ctx, int64_t msg_index) {

@@ -30,8 +30,10 @@ BLOCK_SIZE = 16
 MGR_EXPORTED = ("kvt_mgr_append", "kvt_mgr_begin_request", "kvt_mgr_create", "kvt_mgr_destroy", "kvt_mgr_end_request",
                 "kvt_mgr_entry_tier", "kvt_mgr_fork", "kvt_mgr_free_pages", "kvt_mgr_live_entries",
                 "kvt_mgr_message_pages", "kvt_mgr_message_state", "kvt_mgr_one_off", "kvt_mgr_pin",
-                "kvt_mgr_prefill_done", "kvt_mgr_remove", "kvt_mgr_replace", "kvt_mgr_spawn", "kvt_mgr_start_prefill",
-                "kvt_mgr_terminate", "kvt_mgr_unpin")
+                "kvt_mgr_prefill_done", "kvt_mgr_remove", "kvt_mgr_replace", "kvt_mgr_replay", "kvt_mgr_spawn",
+                "kvt_mgr_start_prefill", "kvt_mgr_terminate", "kvt_mgr_unpin")
+MGR_OPS = ("spawn", "fork", "append", "one_off", "pin", "unpin", "replace", "remove", "terminate", "begin_request",
+           "start_prefill", "prefill_done", "end_request")   # KVT_MGR_OP_* in this order
 EXPORTED = ("kvt_append_kv", "kvt_cascade_extend_attention", "kvt_cascade_workspace_bytes", "kvt_copy_blocks",
             "kvt_decode_attention", "kvt_decode_workspace_bytes", "kvt_extend_attention",
             "kvt_extend_workspace_bytes", "kvt_last_hip_error", "kvt_status_str") + MGR_EXPORTED
@@ -114,6 +116,7 @@ def lib():
             getattr(L, name).argtypes, getattr(L, name).restype = [M] + args, ctypes.c_int
         for name in ("kvt_mgr_message_state", "kvt_mgr_entry_tier"):
             getattr(L, name).argtypes, getattr(L, name).restype = [M, I64, I64], I32
+        L.kvt_mgr_replay.argtypes, L.kvt_mgr_replay.restype = [M, P(I64), I64, P(KvtMgrReport)], I64
         L.kvt_mgr_message_pages.argtypes = [M, I64, I64, P(I32), I64]
         L.kvt_mgr_message_pages.restype = I64
         L.kvt_status_str.argtypes = [ctypes.c_int]
@@ -381,6 +384,26 @@ class Manager:
 
     def prefill_done(self, ctx) -> dict:
         return self._report("kvt_mgr_prefill_done", ctx)
+
+    @staticmethod
+    def encode(events) -> np.ndarray:
+        """(method name, args) pairs as the int64 [n][4] array replay takes."""
+        arr = np.zeros((len(events), 4), dtype=np.int64)
+        for i, (op, args) in enumerate(events):
+            arr[i, 0] = MGR_OPS.index(op)
+            arr[i, 1:1 + len(args)] = args
+        return arr
+
+    def replay(self, events) -> tuple:
+        """Run an encoded event array natively; returns (calls that succeeded,
+        summed start_prefill / prefill_done reports)."""
+        arr = np.ascontiguousarray(events, dtype=np.int64).reshape(-1, 4)
+        rep = KvtMgrReport()
+        ok = int(lib().kvt_mgr_replay(self._h, arr.ctypes.data_as(ctypes.POINTER(ctypes.c_int64)), arr.shape[0],
+                                      ctypes.byref(rep)))
+        if ok < 0:
+            raise ValueError("kvt_mgr_replay rejected its arguments")
+        return ok, rep.as_dict()
 
     def free_pages(self) -> int:
         return int(lib().kvt_mgr_free_pages(self._h))

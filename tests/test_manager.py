@@ -26,6 +26,8 @@ from paper_2609_39819_amd import kvt
 
 PINNED, ACTIVE, SUSPENDED, EXPIRED, TEMPORARY = 0, 1, 2, 3, 4
 T_PINNED, T_ACTIVE, T_SUSPENDED, T_DISCARDED = 0, 1, 2, 3
+REPORT_KEYS = ("admitted_entries", "admitted_pages", "bypassed_entries", "rejected_entries", "released_entries",
+               "released_pages", "hit_tokens", "miss_tokens")
 
 
 def test_state_codes_match_the_header():
@@ -303,6 +305,35 @@ def test_pool_sizes_across_bitmap_words(pages):
     assert o.free_pages() == lib.free_pages()
 
 
+def test_replay_equals_the_calls_one_by_one():
+    """kvt_mgr_replay runs an encoded trace exactly as the calls would: the
+    same successes, summed reports, free pages and final page ids."""
+    from paper_2609_39819_amd.workloads import agent_events
+    events = list(agent_events(seed=3, agents=40, concurrency=10))
+    events += [("pin", (10**6, 0)), ("append", (0, 0)), ("fork", (0, 0))]       # three that fail
+    one, rep = kvt.Manager(2048), kvt.Manager(2048)
+    ok1, tot = 0, {k: 0 for k in REPORT_KEYS}
+    for op, args in events:
+        try:
+            r = getattr(one, op)(*args)
+        except kvt.KvtError:
+            continue
+        ok1 += 1
+        for k in tot:
+            tot[k] += (r or {}).get(k, 0)
+    ok2, tot2 = rep.replay(kvt.Manager.encode(events))
+    assert (ok2, tot2) == (ok1, tot) and ok1 == len(events) - 3
+    assert one.free_pages() == rep.free_pages()
+    for c in range(200):
+        for i in range(60):
+            assert one.message_pages(c, i) == rep.message_pages(c, i)
+    bad = np.array([[99, 0, 0, 0]], dtype=np.int64)                             # unknown op: skipped
+    assert rep.replay(bad) == (0, {k: 0 for k in REPORT_KEYS})
+    assert kvt.lib().kvt_mgr_replay(None, None, 0, None) == -1
+    assert kvt.lib().kvt_mgr_replay(rep._h, None, 1, None) == -1
+    assert kvt.lib().kvt_mgr_replay(rep._h, None, 0, None) == 0
+
+
 def test_manager_bounds():
     lib = kvt.Manager(4)
     lib.spawn(1)
@@ -551,8 +582,6 @@ def test_the_properties_catch_planted_mistakes(planted):
 # the same C++ source under AddressSanitizer and UBSan (host compiler)
 # ---------------------------------------------------------------------------
 
-REPORT_KEYS = ("admitted_entries", "admitted_pages", "bypassed_entries", "rejected_entries", "released_entries",
-               "released_pages", "hit_tokens", "miss_tokens")
 
 
 def _replay_line(m, op, args):
