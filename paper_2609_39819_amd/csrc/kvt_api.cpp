@@ -10,6 +10,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstring>
 #include <numeric>
@@ -30,20 +31,21 @@ kvt_status device_error(hipError_t e) {
 
 int elem_bytes(int32_t dtype) { return dtype == KVT_DTYPE_BF16 ? 2 : 4; }
 
-// Number of compute units of the current device, queried once per device.
+// Number of compute units of the current device, queried once per device
+// (concurrent first calls may both query; they store the same value).
 int device_cus() {
-  static int cached[64] = {0};
+  static std::atomic<int> cached[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) { (void)hipGetLastError(); return 256; }
-  if (cached[dev] == 0) {
-    int n = 0;
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) {
       (void)hipGetLastError();
       n = 256;
     }
-    cached[dev] = n;
+    cached[dev].store(n, std::memory_order_relaxed);
   }
-  return cached[dev];
+  return n;
 }
 
 kvt_status check_pool(const kvt_pool* pool) {

@@ -1,6 +1,8 @@
 // Test driver: replays block-manager calls read from stdin through the C API
-// and prints each call's status and report, one line per call.  Built by
-// tests/test_manager.py with the host compiler and sanitizers.
+// and prints each call's status and report, one line per call; at the end of
+// each stream it replays the same events through kvt_mgr_replay on a fresh
+// manager and prints the summed report.  Built by tests/test_manager.py with
+// the host compiler and sanitizers.
 //
 // Input lines: "<op> <args...>" with op one of spawn fork append one_off pin
 // unpin replace remove terminate begin_request start_prefill prefill_done
@@ -10,10 +12,30 @@
 #include <iostream>
 #include <sstream>
 #include <string>
+#include <vector>
 
 #include "kvt.h"
 
+// the events since the last "pages" line, as kvt_mgr_replay takes them
+static std::vector<int64_t> g_events;
+static long long g_pages = 0;
+
+// replays the collected events on a fresh manager and prints the summary
+static void replay_summary() {
+  if (g_events.empty()) return;
+  kvt_manager* r = kvt_mgr_create(g_pages);
+  kvt_mgr_report tot;
+  const int64_t ok = kvt_mgr_replay(r, g_events.data(), (int64_t)g_events.size() / 4, &tot);
+  std::printf("replay ok=%lld hit=%lld miss=%lld admitted=%lld released=%lld free=%lld\n", (long long)ok,
+              (long long)tot.hit_tokens, (long long)tot.miss_tokens, (long long)tot.admitted_pages,
+              (long long)tot.released_pages, (long long)kvt_mgr_free_pages(r));
+  kvt_mgr_destroy(r);
+  g_events.clear();
+}
+
 int main() {
+  static const char* kOps[] = {"spawn", "fork", "append", "one_off", "pin", "unpin", "replace", "remove",
+                               "terminate", "begin_request", "start_prefill", "prefill_done", "end_request"};
   std::string line;
   kvt_manager* m = nullptr;
   while (std::getline(std::cin, line)) {
@@ -22,11 +44,15 @@ int main() {
     long long a = 0, b = 0, c = 0;
     in >> op >> a >> b >> c;
     if (op == "pages") {
+      replay_summary();
       kvt_mgr_destroy(m);
       m = kvt_mgr_create(a);
+      g_pages = a;
       std::printf("%s\n", m ? "ok" : "null");
       continue;
     }
+    for (int k = 0; k < 13; ++k)
+      if (op == kOps[k]) g_events.insert(g_events.end(), {k, a, b, c});
     kvt_mgr_report rep;
     std::memset(&rep, 0xff, sizeof(rep));
     kvt_status st = KVT_ERR_INVALID_ARG;
@@ -53,6 +79,7 @@ int main() {
                   (long long)rep.miss_tokens);
     std::printf(" free=%lld\n", (long long)kvt_mgr_free_pages(m));
   }
+  replay_summary();
   kvt_mgr_destroy(m);
   return 0;
 }

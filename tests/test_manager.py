@@ -630,14 +630,21 @@ def test_manager_source_is_clean_under_sanitizers(tmp_path):
     streams += [(4096, trace), (1 << 15, trace)]
 
     text, want = [], []
-    for pages, evs in streams:
+    for k, (pages, evs) in enumerate(streams):
         text.append(f"pages {pages}")
         want.append("ok")
         lib = kvt.Manager(pages)
         for op, args in evs:
             text.append(" ".join([op] + [str(a) for a in args]))
             want.append(_replay_line(lib, op, args))
+        ok, tot = kvt.Manager(pages).replay(kvt.Manager.encode(evs))
+        summary = (f"replay ok={ok} hit={tot['hit_tokens']} miss={tot['miss_tokens']} "
+                   f"admitted={tot['admitted_pages']} released={tot['released_pages']} free={lib.free_pages()}")
         lib.close()
+        if k > 0:
+            want.insert(len(want) - len(evs) - 1, prev_summary)
+        prev_summary = summary
+    want.append(prev_summary)
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1:abort_on_error=0", UBSAN_OPTIONS="print_stacktrace=1")
     run = subprocess.run([exe], input="\n".join(text) + "\n", capture_output=True, text=True, env=env, timeout=300)
     assert run.returncode == 0, run.stderr[-3000:]
