@@ -162,6 +162,7 @@ def test_runs_are_bit_identical_and_split_agrees():
     torch.cuda.empty_cache()
 
 
+_edge_rng = np.random.default_rng(560)
 EDGE = [
     # (P, S, Hq, Hkv, D, dtype)
     ([0], [1], 4, 1, 64, "bf16"),
@@ -176,6 +177,10 @@ EDGE = [
     ([2047], [129], 2, 2, 128, "bf16"),
     # 15 key splits; rows 256..306 see no visible key in the last split
     ([15821], [1000], 1, 1, 128, "bf16"),
+    ([300, 4100], [40, 17], 64, 2, 128, "bf16"),     # G = 32: a row tile holds 8 tokens
+    ([2000], [33], 96, 1, 128, "bf16"),              # G = 96: one kv-head for all query heads
+    # 70 sequences: more than one launch's worth of sequence descriptors
+    (_edge_rng.integers(0, 600, size=70).tolist(), _edge_rng.integers(1, 41, size=70).tolist(), 8, 2, 64, "bf16"),
 ]
 
 
