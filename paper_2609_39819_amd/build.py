@@ -1,8 +1,9 @@
 """Build ``libkvt.so`` (the C-ABI library) in-tree with hipcc for gfx950.
 
 ``python -m paper_2609_39819_amd.build`` compiles every source under
-``csrc/`` into objects under ``_build/`` (in parallel) and links
-``paper_2609_39819_amd/libkvt.so`` next to this file.
+``csrc/`` into objects under ``_build/`` (in parallel), links
+``paper_2609_39819_amd/libkvt.so`` next to this file, and builds the tests'
+native caller of the C ABI, ``tests/kvt_run`` (from ``tests/kvt_run.cpp``).
 """
 from __future__ import annotations
 
@@ -18,6 +19,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libkvt.so")
+RUNNER = os.path.join(ROOT, "tests", "kvt_run")   # a native (C++) caller of the C ABI, for the tests
 ARCH = "gfx950"
 
 # Packed fp32 VALU forms are kept out of device code (-packed-fp32-ops).
@@ -59,8 +61,15 @@ def build(verbose: bool = False) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
     os.replace(tmp, LIB)
+    # the native caller used by the tests: host code only, finds the library by rpath
+    cmd = [hipcc(), "-O2", "-std=c++17", "-Wall", "-I", INCLUDE, RUNNER + ".cpp", "-o", RUNNER + ".tmp",
+           "-L", PKG, "-lkvt", "-Wl,-rpath,$ORIGIN/../paper_2609_39819_amd"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"build of {RUNNER} failed: {' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    os.replace(RUNNER + ".tmp", RUNNER)
     if verbose:
-        print(f"built {LIB}")
+        print(f"built {LIB} and {RUNNER}")
     return LIB
 
 
