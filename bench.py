@@ -7,7 +7,7 @@ pages scattered at random over a 2^20-page pool.  Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 
-``--gpus N`` with N > 1 exits: this build measures one GPU only.
+``--gpus N`` with N > 1 exits: the benchmark measures one GPU only.
 """
 from __future__ import annotations
 
@@ -249,7 +249,7 @@ def main():
                     help="page pool of the --manager run (the trace needs about 50K pages to fit)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported by this build", file=sys.stderr)
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported", file=sys.stderr)
         sys.exit(2)
     if args.manager:
         bench_manager(args)

@@ -11,7 +11,7 @@ from oracle import oracle_append, oracle_extend, storage_to_f64
 from paper_2609_39819_amd import kvt
 from paper_2609_39819_amd.workloads import make_config, stage_on_device, torch_to_np
 
-# spec tolerance for bf16 inputs
+# parity tolerance for bf16 inputs
 MAX_ABS = 2e-2
 MEAN_ABS = 2e-3
 
