@@ -96,6 +96,7 @@ bool overlaps(const void* a, size_t an, const void* b, size_t bn) {
 
 struct ExtendPlan {
   int nsplit = 1;
+  int nsplit_shared = 0;    // cascade only: key splits of the shared part
   std::vector<int> order;   // sequences, longest key range first
   size_t ws_bytes = 0;      // workspace needed for nsplit > 1
 };
@@ -186,8 +187,10 @@ kvt_status check_shared(const kvt_seqs* seqs, int32_t shared_len) {
   return KVT_OK;
 }
 
-// Cascade: the split plan of the private parts (prefix lengths less the
-// shared prefix); the workspace holds 1 + nsplit partials per row.
+// Cascade: the split plans of the shared part (one virtual sequence of all T
+// new tokens over the shared keys, all visible) and of the private parts
+// (prefix lengths less the shared prefix); the workspace holds one partial
+// per split of either part.
 ExtendPlan cascade_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shared_len, int32_t num_q_heads,
                         int64_t T) {
   std::vector<int32_t> priv(seqs->num_seqs);
@@ -195,8 +198,14 @@ ExtendPlan cascade_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shar
   kvt_seqs ps = *seqs;
   ps.prefix_len = priv.data();
   ExtendPlan p = make_plan(pool, &ps, num_q_heads, T);
+  const int32_t shared_prefix = shared_len - 1, all_tokens = (int32_t)T;
+  kvt_seqs ss = *seqs;
+  ss.num_seqs = 1;
+  ss.prefix_len = &shared_prefix;
+  ss.suffix_len = &all_tokens;
+  p.nsplit_shared = make_plan(pool, &ss, num_q_heads, T).nsplit;
   const int64_t rows = T * num_q_heads;
-  const int nparts = 1 + p.nsplit;
+  const int nparts = p.nsplit_shared + p.nsplit;
   const size_t o_bytes = (size_t)nparts * rows * pool->head_dim * sizeof(float);
   const size_t ml_bytes = (size_t)nparts * rows * 2 * sizeof(float);
   p.ws_bytes = ((o_bytes + 255) / 256) * 256 + ml_bytes;
@@ -464,31 +473,34 @@ kvt_status kvt_cascade_extend_attention(const kvt_pool* pool, const kvt_seqs* se
 
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const int G = num_q_heads / pool->num_kv_heads;
-  const int nparts = 1 + plan.nsplit;
+  const int nparts = plan.nsplit_shared + plan.nsplit;
   ExtendPlan parts = plan;
-  parts.nsplit = nparts;                       // partial buffers hold the shared part + the splits
+  parts.nsplit = nparts;                       // partial buffers: the shared part's splits, then the private ones
   kvt::ExtendArgs a = base_args(pool, seqs, q, num_q_heads, scale, out, lse, T, parts, workspace);
   a.direct = 0;
 
   // shared part: every new token of the batch against keys [0, shared_len),
   // all of them visible (one virtual sequence whose causal limits start at
-  // shared_len - 1), read through the first sequence's table row
-  a.nsplit = 1;
+  // shared_len - 1), read through the first sequence's table row, with its
+  // own key splits
+  a.nsplit = plan.nsplit_shared;
   a.part_base = 0;
   a.kbeg = 0;
   a.kend = shared_len;
   a.nseq = 1;
   a.seq[0] = kvt::SeqDesc{plan.order[0], shared_len - 1, (int32_t)T, 0};
   a.unit_begin[0] = 0;
-  a.unit_begin[1] = row_tiles((int32_t)T, G);
-  hipError_t e = kvt::launch_extend(a, pool->dtype, pool->head_dim, a.unit_begin[1] * pool->num_kv_heads, s);
+  a.unit_begin[1] = row_tiles((int32_t)T, G) * plan.nsplit_shared;
+  const int64_t shared_grid = (int64_t)a.unit_begin[1] * pool->num_kv_heads;
+  if (shared_grid > INT32_MAX) return KVT_ERR_INVALID_ARG;
+  hipError_t e = kvt::launch_extend(a, pool->dtype, pool->head_dim, (int)shared_grid, s);
   if (e != hipSuccess) return device_error(e);
 
   // private parts: each sequence over keys [shared_len, P_b + i], causal
   std::vector<int32_t> row_off(seqs->num_seqs + 1, 0);
   for (int b = 0; b < seqs->num_seqs; ++b) row_off[b + 1] = row_off[b] + seqs->suffix_len[b];
   a.nsplit = plan.nsplit;
-  a.part_base = 1;
+  a.part_base = plan.nsplit_shared;
   a.kbeg = shared_len;
   a.kend = INT32_MAX;
   for (size_t c0 = 0; c0 < plan.order.size(); c0 += kvt::kSeqsPerLaunch) {

@@ -168,7 +168,7 @@ def test_cascade_workspace_bytes():
     s = _seqs(P=(8192, 20000), S=(2048, 1000), max_blocks=2048)
     ws = kvt.lib().kvt_cascade_workspace_bytes(ctypes.byref(pool), ctypes.byref(s.struct), 4096, 96)
     rows = 3048 * 96
-    parts = ws // (rows * (128 + 2) * 4)       # 1 + key splits of the private parts
+    parts = ws // (rows * (128 + 2) * 4)       # key splits of the shared part + of the private parts
     assert parts >= 2 and ws == -(-parts * rows * 128 * 4 // 256) * 256 + parts * rows * 2 * 4
     assert kvt.lib().kvt_cascade_workspace_bytes(ctypes.byref(pool), ctypes.byref(s.struct), 4100, 96) == 0
 
