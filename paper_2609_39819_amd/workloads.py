@@ -291,7 +291,8 @@ CONFIG_NAMES = ("tiny", "gqa_8k", "react_128k", "forked_agents", "mutation_258k"
 # one GPU's share of the 128K turn under 4-way tensor parallelism (heads split
 # with no communication: 24 query heads over 2 kv-heads per GPU)
 # one decoding step of a batch of 32 agent contexts (one new token each)
-EXTRA_CONFIG_NAMES = ("react_128k_tp4", "decode_batch")
+# 16 forked sub-agents each adding a short message over a long shared context
+EXTRA_CONFIG_NAMES = ("react_128k_tp4", "decode_batch", "forked_short")
 
 
 def config_shapes(name: str) -> dict:
@@ -315,6 +316,10 @@ def config_shapes(name: str) -> dict:
         return dict(seed=4, num_q_heads=96, num_kv_heads=8, head_dim=128, dtype="bf16",
                     num_blocks=1 << 20, num_seqs=16, shared_prefix=4096,
                     private_prefix=(4096, 65536), suffix=(256, 4096))
+    if name == "forked_short":
+        return dict(seed=8, num_q_heads=96, num_kv_heads=8, head_dim=128, dtype="bf16",
+                    num_blocks=1 << 18, num_seqs=16, shared_prefix=32768,
+                    private_prefix=(0, 1023), suffix=(16, 16))
     if name == "mutation_258k":
         return dict(seed=5, num_q_heads=96, num_kv_heads=8, head_dim=128, dtype="bf16",
                     num_blocks=1 << 20, prefix=204800, suffix=57344)
@@ -335,7 +340,7 @@ def forked_lengths(rng: np.random.Generator, num_seqs: int, shared: int, private
 def make_config(name: str, variant: str = "normal", keep_logical: Optional[bool] = None) -> Workload:
     c = config_shapes(name)
     rng = np.random.default_rng(c["seed"])
-    if name == "forked_agents":
+    if name in ("forked_agents", "forked_short"):
         P, S = forked_lengths(rng, c["num_seqs"], c["shared_prefix"], c["private_prefix"], c["suffix"])
         sh_blocks = c["shared_prefix"] // BLOCK_SIZE
     elif name == "decode_batch":

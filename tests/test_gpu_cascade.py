@@ -4,7 +4,8 @@ The cascade computes the same attention as extend (shared keys for the whole
 batch at once, private keys per sequence, log-sum-exp merge), so the
 reference is ``oracle_extend``.  Covered: the forked-agents workload (4096
 shared positions, 16 sequences; sampled rows, lse, agreement with the plain
-extend kernel) and edge shapes: a shared length that is not a multiple of the
+extend kernel), short new messages over a 32768-position shared prefix, and
+edge shapes: a shared length that is not a multiple of the
 64-key tile, a sequence whose whole prefix is shared, a single sequence,
 D = 64, fp32 storage, and key splits in the private parts.
 """
@@ -53,6 +54,27 @@ def test_forked_agents_cascade_matches_oracle():
     compare(gather_rows(to_f64(out, w.dtype), w, rows), ref_o, "forked cascade out")
     compare(gather_rows(lse.cpu().numpy().astype(np.float64), w, rows), ref_l, "forked cascade lse")
     assert bool(torch.isfinite(out.float()).all())
+    plain = run_extend(w, d)
+    compare(to_f64(out, w.dtype), to_f64(plain, w.dtype), "cascade vs extend", max_abs=1e-2, mean_abs=5e-4)
+    del d
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(600)
+def test_short_messages_over_a_long_shared_prefix():
+    """16 sub-agents adding 16 tokens each over 32768 shared positions: the
+    shared pass runs with its own key splits."""
+    w = cached_config("forked_short")
+    shared = config_shapes("forked_short")["shared_prefix"]
+    d = stage(w)
+    run_append(w, d)
+    out, lse = run_cascade(w, d, shared, return_lse=True)
+    rows = sample_rows(w, 8)
+    kp, vp = oracle_pools("forked_short")
+    ref_o, ref_l = oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len, w.suffix_len, w.num_kv_heads, w.scale,
+                                 rows=rows)
+    compare(gather_rows(to_f64(out, w.dtype), w, rows), ref_o, "forked_short cascade out")
+    compare(gather_rows(lse.cpu().numpy().astype(np.float64), w, rows), ref_l, "forked_short cascade lse")
     plain = run_extend(w, d)
     compare(to_f64(out, w.dtype), to_f64(plain, w.dtype), "cascade vs extend", max_abs=1e-2, mean_abs=5e-4)
     del d
