@@ -157,40 +157,37 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
     const int slot = min(keyrow[i] & (kBlock - 1), last);
     return ((((int64_t)id * hkv + g) << 4) + slot) * D + chunk_off[i];
   };
-  // in a tile whose 64 positions all lie inside the sequence, a lane's byte
-  // offset within its page run is a constant over the wave-uniform page base
-  uint32_t lane_byte[NREG];
+  // bf16 storage: global -> LDS by DMA.  A lane's piece lies at a byte offset
+  // within its page run; positions past the end of the sequence take the
+  // offset of the last real position instead (lane_bytes, branch-free).  The
+  // DMAs themselves (dma) carry no branch either, so the score product can
+  // spread them between its matrix instructions instead of every wave
+  // issuing all of them at once.
+  auto lane_bytes = [&](int jn, uint32_t (&lb)[NREG]) __attribute__((always_inline)) {
 #pragma unroll
-  for (int i = 0; i < NREG; ++i) lane_byte[i] = (uint32_t)(((keyrow[i] & (kBlock - 1)) * D + chunk_off[i]) * 2);
-  u32x4 stK[NREG], stV[NREG];   // register staging (fp32 storage only)
-  auto issue = [&](int jn, const uint32_t (&ids)[NREG], const Slot<D>& dst) __attribute__((always_inline)) {
-    if constexpr (kDirect) {
-      if ((jn + 1) * KT <= L) {
-#pragma unroll
-        for (int i = 0; i < NREG; ++i) {
-          const int64_t base = (((int64_t)ids[i] * hkv + g) << 4) * D;
-          const char* ks = reinterpret_cast<const char*>(kpool + base) + lane_byte[i];
-          const char* vs = reinterpret_cast<const char*>(vpool + base) + lane_byte[i];
-          lds_bf16* kd = (lds_bf16*)dst.k.e + lds_off[i];
-          lds_bf16* vd = (lds_bf16*)dst.v.e + lds_off[i];
-          __builtin_amdgcn_global_load_lds((const void*)ks, (__attribute__((address_space(3))) void*)kd, 16, 0, 0);
-          __builtin_amdgcn_global_load_lds((const void*)vs, (__attribute__((address_space(3))) void*)vd, 16, 0, 0);
-        }
-        return;
-      }
+    for (int i = 0; i < NREG; ++i) {
+      const int page = min(jn * 4 + page_in_tile[i], nblk - 1);
+      const int last = L - 1 - page * kBlock;
+      lb[i] = (uint32_t)((min(keyrow[i] & (kBlock - 1), last) * D + chunk_off[i]) * 2);
     }
+  };
+  auto dma = [&](uint32_t id, uint32_t lb, int i, const Slot<D>& dst) __attribute__((always_inline)) {
+    const int64_t base = (((int64_t)id * hkv + g) << 4) * D;
+    const char* ks = reinterpret_cast<const char*>(kpool + base) + lb;
+    const char* vs = reinterpret_cast<const char*>(vpool + base) + lb;
+    lds_bf16* kd = (lds_bf16*)dst.k.e + lds_off[i];
+    lds_bf16* vd = (lds_bf16*)dst.v.e + lds_off[i];
+    __builtin_amdgcn_global_load_lds((const void*)ks, (__attribute__((address_space(3))) void*)kd, 16, 0, 0);
+    __builtin_amdgcn_global_load_lds((const void*)vs, (__attribute__((address_space(3))) void*)vd, 16, 0, 0);
+  };
+  // fp32 storage: loads through registers (rounded to bf16), stored once they land
+  u32x4 stK[NREG], stV[NREG];
+  auto issue_staged = [&](int jn, const uint32_t (&ids)[NREG]) __attribute__((always_inline)) {
 #pragma unroll
     for (int i = 0; i < NREG; ++i) {
       const int64_t off = src_off(jn, i, ids[i]);
-      if constexpr (kDirect) {
-        lds_bf16* kd = (lds_bf16*)dst.k.e + lds_off[i];
-        lds_bf16* vd = (lds_bf16*)dst.v.e + lds_off[i];
-        __builtin_amdgcn_global_load_lds((const void*)(kpool + off), (__attribute__((address_space(3))) void*)kd, 16, 0, 0);
-        __builtin_amdgcn_global_load_lds((const void*)(vpool + off), (__attribute__((address_space(3))) void*)vd, 16, 0, 0);
-      } else {
-        stK[i] = load8(kpool + off);
-        stV[i] = load8(vpool + off);
-      }
+      stK[i] = load8(kpool + off);
+      stV[i] = load8(vpool + off);
     }
   };
   auto stash = [&](const Slot<D>& dst) __attribute__((always_inline)) {
@@ -231,9 +228,16 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
       voff[dt][r2] = key * D + (((dcol >> 3) ^ swz<D>(key)) << 3) + (dcol & 7);
     }
   // ---- S^T = K Q^T of one tile: two independent 32-key accumulator chains
-  // per 32-row block, each K fragment read from LDS feeding NB blocks
-  auto qk = [&](const Slot<D>& tl, f32x16 (&s)[NB][2]) __attribute__((always_inline)) {
+  // per 32-row block, each K fragment read from LDS feeding NB blocks.  With
+  // bf16 storage it also issues the gather of the next tile into `fill`
+  // (page ids, lane offsets lb), one DMA after each of score steps 1 .. 2*NREG.
+  auto qk = [&](const Slot<D>& tl, f32x16 (&s)[NB][2], const uint32_t (&ids)[NREG], const uint32_t (&lb)[NREG],
+                const Slot<D>& fill) __attribute__((always_inline)) {
     const __bf16* ks = tl.k.e;
+    if constexpr (kDirect) {
+#pragma unroll
+      for (int i = 0; i < NREG; ++i) dma(ids[i], lb[i], i, fill);
+    }
 #pragma unroll
     for (int b = 0; b < NB; ++b) s[b][0] = s[b][1] = (f32x16){};
     bf16x8 kf[KSTEPS][2];
@@ -251,12 +255,14 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
       }
     }
     // K fragments read ahead of the products that use them: two steps'
-    // worth first, then each pair of products followed by the next pair of reads
+    // worth first, then each pair of products followed by the next pair of
+    // reads and (after steps 1 .. 2*NREG) one gather DMA
     __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
     for (int kk = 0; kk < KSTEPS - 2; ++kk) {
       __builtin_amdgcn_sched_group_barrier(0x008, 2 * NB, 0);
       __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      if (kDirect && kk >= 1 && kk <= 2 * NREG) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
     }
     __builtin_amdgcn_sched_group_barrier(0x008, 4 * NB, 0);
   };
@@ -358,27 +364,39 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
     }
   };
 
-  // ---- main loop.  Step t first starts the gather of tile t+1 into the
-  // other slot (its page ids were fetched a step earlier), then computes
-  // tile t: scores, settle, probabilities, value product.  The wait + barrier
-  // at the end publishes tile t+1 and frees the slot of tile t for the
-  // gather of tile t+2.
+  // ---- main loop.  Step t computes tile t (scores, settle, probabilities,
+  // value product) and, inside the score product, gathers tile t+1 into the
+  // other slot (its page ids were fetched a step earlier; past the last
+  // tile the gather still reads clamped, in-bounds pages into a slot no one
+  // reads).  The wait + barrier at the end publishes tile t+1 and frees the
+  // slot of tile t for the gather of tile t+2.
   const int n = j1 - j0;
-  uint32_t ids[NREG];
+  uint32_t ids[NREG], lb[NREG];
   page_ids(j0, ids);
-  if (n > 0) { issue(j0, ids, tile0); stash(tile0); }
+  if (n > 0) {
+    if constexpr (kDirect) {
+      lane_bytes(j0, lb);
+#pragma unroll
+      for (int i = 0; i < NREG; ++i) dma(ids[i], lb[i], i, tile0);
+    } else {
+      issue_staged(j0, ids);
+      stash(tile0);
+    }
+  }
   page_ids(j0 + 1, ids);
   __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
   __syncthreads();
   f32x16 s_cur[NB][2];
   bf16x8 pb[NB][4];
   auto step = [&](int t, const Slot<D>& cur, const Slot<D>& fill) __attribute__((always_inline)) {
-    if (t + 1 < n) {
-      issue(j0 + t + 1, ids, fill);
+    if constexpr (kDirect) {
+      lane_bytes(j0 + t + 1, lb);
+    } else if (t + 1 < n) {
+      issue_staged(j0 + t + 1, ids);
       stash(fill);
-      page_ids(j0 + t + 2, ids);
     }
-    qk(cur, s_cur);
+    qk(cur, s_cur, ids, lb, fill);
+    page_ids(j0 + t + 2, ids);
     settle(j0 + t, s_cur);
     probs(s_cur, pb);
     pv(cur, pb);
