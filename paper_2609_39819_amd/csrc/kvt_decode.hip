@@ -115,8 +115,13 @@ __global__ __launch_bounds__(kWaves * 64) void decode_kernel(const ExtendArgs a)
       const int page = min(j * 2 + p, nblk - 1);
       const int slot = min((RPR * i + lane / CHUNKS) & (kBlock - 1), L - 1 - page * kBlock);
       const int64_t off = ((((int64_t)ids[p] * hkv + g) << 4) + slot) * D + chunk_off[i];
-      st.k[i] = load8(kpool + off);
-      st.v[i] = load8(vpool + off);
+      if constexpr (sizeof(T) == 2) {   // each page is read once: nontemporal loads
+        st.k[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(kpool + off));
+        st.v[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(vpool + off));
+      } else {
+        st.k[i] = load8(kpool + off);
+        st.v[i] = load8(vpool + off);
+      }
     }
   };
   auto stash = [&](const Stage& st, DecSlot<D>& dst) __attribute__((always_inline)) {
