@@ -110,7 +110,8 @@ kvt_status kvt_append_kv(const kvt_pool* pool, const kvt_seqs* seqs,
  * be enqueued first (same stream, or otherwise ordered before this call).
  *
  * q: device [T][Hq][D]; out: device [T][Hq][D] (may not overlap q or a pool);
- * lse: device float [T][Hq] or NULL.  num_q_heads must be a multiple of Hkv.
+ * lse: device float [T][Hq] or NULL.  num_q_heads must be a multiple of Hkv,
+ * and T * num_q_heads at most INT32_MAX (else KVT_ERR_INVALID_ARG).
  * scale: finite and > 0 (usually 1/sqrt(D)).
  * workspace: device scratch for split-key partial results.  Pass NULL/0 to
  * run without splitting; otherwise workspace_bytes must be at least

@@ -76,6 +76,13 @@ kvt_status check_seqs(const kvt_seqs* seqs, int64_t* total_tokens) {
   return KVT_OK;
 }
 
+// Query heads: a positive multiple of the kv-heads, and T * num_q_heads
+// packed query rows must fit the kernels' 32-bit row indices.
+bool heads_ok(const kvt_pool* pool, int32_t num_q_heads, int64_t T) {
+  if (num_q_heads < 1 || num_q_heads % pool->num_kv_heads != 0) return false;
+  return T * num_q_heads <= INT32_MAX;
+}
+
 // Checked mode: every used block id is inside the pool.
 kvt_status check_table_ids(const kvt_pool* pool, const kvt_seqs* seqs) {
   if (seqs->block_table_host == nullptr) return KVT_OK;
@@ -349,7 +356,7 @@ size_t kvt_extend_workspace_bytes(const kvt_pool* pool, const kvt_seqs* seqs, in
   if (check_pool(pool) != KVT_OK) return 0;
   int64_t T = 0;
   if (check_seqs(seqs, &T) != KVT_OK) return 0;
-  if (num_q_heads < 1 || num_q_heads % pool->num_kv_heads != 0) return 0;
+  if (!heads_ok(pool, num_q_heads, T)) return 0;
   return make_plan(pool, seqs, num_q_heads, T).ws_bytes;
 }
 
@@ -361,7 +368,7 @@ kvt_status kvt_extend_attention(const kvt_pool* pool, const kvt_seqs* seqs, cons
   int64_t T = 0;
   if ((st = check_seqs(seqs, &T)) != KVT_OK) return st;
   if (q == nullptr || out == nullptr) return KVT_ERR_INVALID_ARG;
-  if (num_q_heads < 1 || num_q_heads % pool->num_kv_heads != 0) return KVT_ERR_INVALID_ARG;
+  if (!heads_ok(pool, num_q_heads, T)) return KVT_ERR_INVALID_ARG;
   if (!(scale > 0.f) || !std::isfinite(scale)) return KVT_ERR_INVALID_ARG;
   if ((st = check_table_ids(pool, seqs)) != KVT_OK) return st;
   if ((st = check_outputs(pool, q, num_q_heads, out, lse, T)) != KVT_OK) return st;
@@ -448,7 +455,7 @@ size_t kvt_cascade_workspace_bytes(const kvt_pool* pool, const kvt_seqs* seqs, i
   if (check_pool(pool) != KVT_OK) return 0;
   int64_t T = 0;
   if (check_seqs(seqs, &T) != KVT_OK) return 0;
-  if (num_q_heads < 1 || num_q_heads % pool->num_kv_heads != 0) return 0;
+  if (!heads_ok(pool, num_q_heads, T)) return 0;
   if (check_shared(seqs, shared_len) != KVT_OK) return 0;
   return cascade_plan(pool, seqs, shared_len, num_q_heads, T).ws_bytes;
 }
@@ -464,7 +471,7 @@ kvt_status kvt_cascade_extend_attention(const kvt_pool* pool, const kvt_seqs* se
   if (workspace == nullptr && workspace_bytes == 0)   // no scratch: the plain extend computes the same
     return kvt_extend_attention(pool, seqs, q, num_q_heads, scale, out, lse, nullptr, 0, stream);
   if (q == nullptr || out == nullptr) return KVT_ERR_INVALID_ARG;
-  if (num_q_heads < 1 || num_q_heads % pool->num_kv_heads != 0) return KVT_ERR_INVALID_ARG;
+  if (!heads_ok(pool, num_q_heads, T)) return KVT_ERR_INVALID_ARG;
   if (!(scale > 0.f) || !std::isfinite(scale)) return KVT_ERR_INVALID_ARG;
   if ((st = check_table_ids(pool, seqs)) != KVT_OK) return st;
   if ((st = check_outputs(pool, q, num_q_heads, out, lse, T)) != KVT_OK) return st;
@@ -526,7 +533,7 @@ size_t kvt_decode_workspace_bytes(const kvt_pool* pool, const kvt_seqs* seqs, in
   if (check_pool(pool) != KVT_OK) return 0;
   int64_t T = 0;
   if (check_seqs(seqs, &T) != KVT_OK || T != seqs->num_seqs) return 0;
-  if (num_q_heads < 1 || num_q_heads % pool->num_kv_heads != 0) return 0;
+  if (!heads_ok(pool, num_q_heads, T)) return 0;
   if (num_q_heads / pool->num_kv_heads > kvt::kDecMaxGroup) return 0;
   return make_decode_plan(pool, seqs, num_q_heads).ws_bytes;
 }
@@ -540,7 +547,7 @@ kvt_status kvt_decode_attention(const kvt_pool* pool, const kvt_seqs* seqs, cons
   if ((st = check_seqs(seqs, &T)) != KVT_OK) return st;
   if (T != seqs->num_seqs) return KVT_ERR_INVALID_ARG;   // one new token per sequence
   if (q == nullptr || out == nullptr) return KVT_ERR_INVALID_ARG;
-  if (num_q_heads < 1 || num_q_heads % pool->num_kv_heads != 0) return KVT_ERR_INVALID_ARG;
+  if (!heads_ok(pool, num_q_heads, T)) return KVT_ERR_INVALID_ARG;
   if (num_q_heads / pool->num_kv_heads > kvt::kDecMaxGroup) return KVT_ERR_UNSUPPORTED;
   if (!(scale > 0.f) || !std::isfinite(scale)) return KVT_ERR_INVALID_ARG;
   if ((st = check_table_ids(pool, seqs)) != KVT_OK) return st;

@@ -126,6 +126,12 @@ def test_extend_specific_checks():
     assert _extend(_pool(), _seqs(), scale=float("inf")) == E
     assert _extend(_pool(), _seqs(), out=FAKE_Q + 64) == E           # out overlaps q
     assert _extend(_pool(), _seqs(), out=FAKE_K + 128) == E          # out inside the K pool
+    # 2^24 new tokens x 128 query heads = 2^31 packed rows: past the kernels' 32-bit row indices
+    big = _seqs(P=(0,), S=(1 << 24,), max_blocks=1 << 20)
+    assert _extend(_pool(nb=1 << 20), big, hq=128) == E
+    assert _extend(_pool(nb=1 << 20), big, hq=128, ws=0x60000000000, ws_bytes=1 << 40) == E
+    pool = _pool(nb=1 << 20)
+    assert kvt.lib().kvt_extend_workspace_bytes(ctypes.byref(pool), ctypes.byref(big.struct), 128) == 0
 
 
 @no_gpu_only
