@@ -89,7 +89,8 @@ typedef struct {
  *
  * For every b, t < S_b, kv-head g, with p = P_b + t:
  *   k_pool[block_table[b][p/16]][g][p%16][:] = k_new[off_b + t][g][:]  (same for v)
- * a bitwise copy.  k_new, v_new: device [T][Hkv][D] in the pool dtype.
+ * a bitwise copy.  k_new, v_new: device [T][Hkv][D] in the pool dtype; they
+ * and the pools must be 16-byte aligned (else KVT_ERR_INVALID_ARG).
  * No other pool byte is written.  Targets must be distinct across the call
  * (checked mode rejects a repeated (block, slot) with KVT_ERR_OUT_OF_RANGE);
  * blocks shared by several sequences (a fork) are read-only here as long as
@@ -112,6 +113,8 @@ kvt_status kvt_append_kv(const kvt_pool* pool, const kvt_seqs* seqs,
  * q: device [T][Hq][D]; out: device [T][Hq][D] (may not overlap q or a pool);
  * lse: device float [T][Hq] or NULL.  num_q_heads must be a multiple of Hkv,
  * and T * num_q_heads at most INT32_MAX (else KVT_ERR_INVALID_ARG).
+ * q, out, the pools and the workspace must be 16-byte aligned, lse 4-byte
+ * aligned (else KVT_ERR_INVALID_ARG); fresh device allocations are.
  * scale: finite and > 0 (usually 1/sqrt(D)).
  * workspace: device scratch for split-key partial results.  Pass NULL/0 to
  * run without splitting; otherwise workspace_bytes must be at least

@@ -48,8 +48,12 @@ int device_cus() {
   return n;
 }
 
+// The kernels move 16-byte pieces of every token row, page and workspace.
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
 kvt_status check_pool(const kvt_pool* pool) {
   if (pool == nullptr || pool->k == nullptr || pool->v == nullptr) return KVT_ERR_INVALID_ARG;
+  if (!aligned16(pool->k) || !aligned16(pool->v)) return KVT_ERR_INVALID_ARG;
   if (pool->num_blocks < 1 || pool->num_kv_heads < 1) return KVT_ERR_INVALID_ARG;
   if (pool->head_dim != 64 && pool->head_dim != 128) return KVT_ERR_UNSUPPORTED;
   if (pool->dtype != KVT_DTYPE_BF16 && pool->dtype != KVT_DTYPE_F32) return KVT_ERR_UNSUPPORTED;
@@ -101,6 +105,15 @@ bool overlaps(const void* a, size_t an, const void* b, size_t bn) {
   return x < y + bn && y < x + an;
 }
 
+// Workspace of nsplit partial results per packed row: the unnormalised
+// outputs in fp32 (256-byte aligned block), then (m, l) in fp32.
+size_t part_o_bytes(const kvt_pool* pool, int nsplit, int64_t rows) {
+  return (((size_t)nsplit * rows * pool->head_dim * sizeof(float) + 255) / 256) * 256;
+}
+size_t part_bytes(const kvt_pool* pool, int nsplit, int64_t rows) {
+  return part_o_bytes(pool, nsplit, rows) + (size_t)nsplit * rows * 2 * sizeof(float);
+}
+
 struct ExtendPlan {
   int nsplit = 1;
   int nsplit_shared = 0;    // cascade only: key splits of the shared part
@@ -143,12 +156,7 @@ ExtendPlan make_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t num_q_h
     if (rounds(s) < rounds(ns) - 1e-9) ns = s;
   if (rounds(ns) > 0.9 * rounds(1)) ns = 1;
   p.nsplit = ns;
-  if (ns > 1) {
-    const int64_t rows = T * num_q_heads;
-    const size_t o_bytes = (size_t)ns * rows * pool->head_dim * sizeof(float);
-    const size_t ml_bytes = (size_t)ns * rows * 2 * sizeof(float);
-    p.ws_bytes = ((o_bytes + 255) / 256) * 256 + ml_bytes;
-  }
+  if (ns > 1) p.ws_bytes = part_bytes(pool, ns, T * num_q_heads);
   return p;
 }
 
@@ -169,12 +177,7 @@ ExtendPlan make_decode_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t 
   const int64_t want = (2 * (int64_t)device_cus() + units - 1) / units;
   const int64_t by_keys = std::max<int64_t>(1, min_keys / 1024);
   p.nsplit = (int)std::max<int64_t>(1, std::min<int64_t>({want, by_keys, (int64_t)kvt::kMaxSplits}));
-  if (p.nsplit > 1) {
-    const int64_t rows = (int64_t)B * num_q_heads;
-    const size_t o_bytes = (size_t)p.nsplit * rows * pool->head_dim * sizeof(float);
-    const size_t ml_bytes = (size_t)p.nsplit * rows * 2 * sizeof(float);
-    p.ws_bytes = ((o_bytes + 255) / 256) * 256 + ml_bytes;
-  }
+  if (p.nsplit > 1) p.ws_bytes = part_bytes(pool, p.nsplit, (int64_t)B * num_q_heads);
   return p;
 }
 
@@ -211,17 +214,14 @@ ExtendPlan cascade_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shar
   ss.prefix_len = &shared_prefix;
   ss.suffix_len = &all_tokens;
   p.nsplit_shared = make_plan(pool, &ss, num_q_heads, T).nsplit;
-  const int64_t rows = T * num_q_heads;
-  const int nparts = p.nsplit_shared + p.nsplit;
-  const size_t o_bytes = (size_t)nparts * rows * pool->head_dim * sizeof(float);
-  const size_t ml_bytes = (size_t)nparts * rows * 2 * sizeof(float);
-  p.ws_bytes = ((o_bytes + 255) / 256) * 256 + ml_bytes;
+  p.ws_bytes = part_bytes(pool, p.nsplit_shared + p.nsplit, T * num_q_heads);
   return p;
 }
 
 // out must not overlap q or a pool; lse must not overlap out.
 kvt_status check_outputs(const kvt_pool* pool, const void* q, int32_t num_q_heads, const void* out,
                          const float* lse, int64_t T) {
+  if (!aligned16(q) || !aligned16(out) || ((uintptr_t)lse & 3) != 0) return KVT_ERR_INVALID_ARG;
   const size_t es = elem_bytes(pool->dtype);
   const size_t tok_bytes = (size_t)T * num_q_heads * pool->head_dim * es;
   const size_t pool_bytes = (size_t)pool->num_blocks * pool->num_kv_heads * kvt::kBlock * pool->head_dim * es;
@@ -257,9 +257,9 @@ kvt::ExtendArgs base_args(const kvt_pool* pool, const kvt_seqs* seqs, const void
   a.nsplit = plan.nsplit;
   a.total_rows = (int32_t)T;
   if (plan.nsplit > 1) {
-    const size_t o_bytes = (size_t)plan.nsplit * T * num_q_heads * pool->head_dim * sizeof(float);
     a.part_o = reinterpret_cast<float*>(workspace);
-    a.part_ml = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) + ((o_bytes + 255) / 256) * 256);
+    a.part_ml = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) +
+                                         part_o_bytes(pool, plan.nsplit, T * num_q_heads));
   }
   return a;
 }
@@ -302,7 +302,7 @@ kvt_status kvt_append_kv(const kvt_pool* pool, const kvt_seqs* seqs, const void*
   if (st != KVT_OK) return st;
   int64_t T = 0;
   if ((st = check_seqs(seqs, &T)) != KVT_OK) return st;
-  if (k_new == nullptr || v_new == nullptr) return KVT_ERR_INVALID_ARG;
+  if (k_new == nullptr || v_new == nullptr || !aligned16(k_new) || !aligned16(v_new)) return KVT_ERR_INVALID_ARG;
   if ((st = check_table_ids(pool, seqs)) != KVT_OK) return st;
   const size_t pool_bytes = (size_t)pool->num_blocks * pool->num_kv_heads * kvt::kBlock * pool->head_dim *
                             elem_bytes(pool->dtype);
@@ -379,6 +379,8 @@ kvt_status kvt_extend_attention(const kvt_pool* pool, const kvt_seqs* seqs, cons
       plan.nsplit = 1;   // no scratch offered: run unsplit
     } else if (workspace == nullptr || workspace_bytes < plan.ws_bytes) {
       return KVT_ERR_WORKSPACE;
+    } else if (!aligned16(workspace)) {
+      return KVT_ERR_INVALID_ARG;
     }
   }
 
@@ -477,6 +479,7 @@ kvt_status kvt_cascade_extend_attention(const kvt_pool* pool, const kvt_seqs* se
   if ((st = check_outputs(pool, q, num_q_heads, out, lse, T)) != KVT_OK) return st;
   const ExtendPlan plan = cascade_plan(pool, seqs, shared_len, num_q_heads, T);
   if (workspace == nullptr || workspace_bytes < plan.ws_bytes) return KVT_ERR_WORKSPACE;
+  if (!aligned16(workspace)) return KVT_ERR_INVALID_ARG;
 
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const int G = num_q_heads / pool->num_kv_heads;
@@ -559,6 +562,8 @@ kvt_status kvt_decode_attention(const kvt_pool* pool, const kvt_seqs* seqs, cons
       plan.nsplit = 1;
     } else if (workspace == nullptr || workspace_bytes < plan.ws_bytes) {
       return KVT_ERR_WORKSPACE;
+    } else if (!aligned16(workspace)) {
+      return KVT_ERR_INVALID_ARG;
     }
   }
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);

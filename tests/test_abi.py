@@ -132,6 +132,15 @@ def test_extend_specific_checks():
     assert _extend(_pool(nb=1 << 20), big, hq=128, ws=0x60000000000, ws_bytes=1 << 40) == E
     pool = _pool(nb=1 << 20)
     assert kvt.lib().kvt_extend_workspace_bytes(ctypes.byref(pool), ctypes.byref(big.struct), 128) == 0
+    # device buffers must be 16-byte aligned (lse 4-byte)
+    assert _extend(_pool(), _seqs(), q=FAKE_Q + 8) == E
+    assert _extend(_pool(), _seqs(), out=FAKE_OUT + 8) == E
+    assert _extend(_pool(k=FAKE_K + 8), _seqs()) == E
+    assert kvt.lib().kvt_extend_attention(ctypes.byref(_pool()), ctypes.byref(_seqs().struct), FAKE_Q, 4, 0.125,
+                                          FAKE_OUT, FAKE_OUT + (1 << 30) + 2, None, 0, None) == E
+    s8k = _seqs(P=(8192,), S=(512,), max_blocks=544)
+    assert _extend(_pool(nb=65536, hkv=8, d=128), s8k, hq=32, ws=0x60000000008, ws_bytes=1 << 30) == E
+    assert _append(_pool(), _seqs(), kn=FAKE_Q + 4) == E
 
 
 @no_gpu_only
