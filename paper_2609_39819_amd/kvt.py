@@ -135,9 +135,17 @@ def status_str(s: int) -> str:
 # raw structs (plain integers as pointers)
 # ---------------------------------------------------------------------------
 
+_I32_MIN, _I32_MAX = -(1 << 31), (1 << 31) - 1
+
+
 def _i32_array(x) -> ctypes.Array:
+    # short lists of Python ints (the common case: a few sequence lengths)
+    # skip numpy; anything else goes through it, which rejects values
+    # outside int32 instead of wrapping them
+    if type(x) in (list, tuple) and len(x) <= 64 and all(type(e) is int and _I32_MIN <= e <= _I32_MAX for e in x):
+        return (ctypes.c_int32 * len(x))(*x)
     a = np.ascontiguousarray(np.asarray(x, dtype=np.int32).reshape(-1))
-    return (ctypes.c_int32 * a.size)(*a.tolist())
+    return (ctypes.c_int32 * a.size).from_buffer_copy(a)
 
 
 def raw_pool(k: int, v: int, num_blocks: int, num_kv_heads: int, head_dim: int, dtype: int) -> KvtPool:
@@ -203,7 +211,7 @@ def append_kv(k_pool, v_pool, block_table, prefix_len: Sequence[int], suffix_len
     """Scatter the new tokens' K/V into their pages (``kvt_append_kv``)."""
     pool = _pool_struct(k_pool, v_pool)
     seqs = _seqs(prefix_len, suffix_len, block_table, checked)
-    T = int(np.sum(np.asarray(suffix_len, dtype=np.int64)))
+    T = sum(seqs.suffix)
     _check_tokens(k_new, "k_new", T, pool.num_kv_heads, pool.head_dim, k_pool.dtype)
     _check_tokens(v_new, "v_new", T, pool.num_kv_heads, pool.head_dim, k_pool.dtype)
     st = lib().kvt_append_kv(ctypes.byref(pool), ctypes.byref(seqs.struct), k_new.data_ptr(), v_new.data_ptr(),
@@ -299,7 +307,7 @@ def _attention(entry: str, ws_entry: str, q, k_pool, v_pool, block_table, prefix
     lead = () if shared is None else (shared,)   # the cascade entry points take shared_len after seqs
     pool = _pool_struct(k_pool, v_pool)
     seqs = _seqs(prefix_len, suffix_len, block_table, checked)
-    T = int(np.sum(np.asarray(suffix_len, dtype=np.int64)))
+    T = sum(seqs.suffix)
     Hq = int(q.shape[1])
     _check_tokens(q, "q", T, Hq, pool.head_dim, k_pool.dtype)
     if scale is None:
