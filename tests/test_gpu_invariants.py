@@ -11,7 +11,8 @@
   of extend(P, S1 + S2) within tolerance;
 * fork sharing: sequences that share their first pages (a forked context,
   §5.2, §6.1) give bit-identical results to the same batch with private
-  copies of those pages.
+  copies of those pages;
+* the decoding step obeys the first and last of these as well.
 """
 import numpy as np
 import pytest
@@ -152,3 +153,53 @@ def test_fork_sharing_is_bit_identical_to_private_copies():
     kp, vp = oracle_append(w.k_pool_c, w.v_pool_c, w.compact_table, w.prefix_len, w.suffix_len, w.k_new, w.v_new)
     ref, _ = oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len, w.suffix_len, w.num_kv_heads, w.scale)
     compare(to_f64(o1, w.dtype), ref, "forked batch vs oracle")
+
+
+@pytest.mark.timeout(300)
+def test_decode_is_invisible_to_paging_and_fork_sharing():
+    """One decoding step (one new token per sequence, key splits over the
+    long contexts): relabelling every page, and private copies of a shared
+    prefix, leave out and lse bit-identical."""
+    sh = 32
+    P, S = [6000, 2700, 3333, 2048], [1, 1, 1, 1]     # >= 2048 keys each: two key splits
+    w = build_workload(name="decode-inv", seed=9305, prefix_len=P, suffix_len=S, num_q_heads=32, num_kv_heads=4,
+                       head_dim=128, dtype="bf16", shared_prefix_blocks=sh,
+                       num_blocks=pages_needed(P, S, sh) + 3 * sh + 50)
+    d = stage(w)
+    append(d, w, w.prefix_len, w.suffix_len, d["k_new"], d["v_new"])
+
+    def decode(pools=None, table=None):
+        kp, vp = pools if pools is not None else (d["k_pool"], d["v_pool"])
+        r = kvt.decode_attention(d["q"], kp, vp, d["block_table"] if table is None else table, w.prefix_len,
+                                 w.scale, return_lse=True, checked=True)
+        torch.cuda.synchronize()
+        return r
+
+    o1, l1 = decode()
+    perm = torch.randperm(w.num_blocks, generator=torch.Generator().manual_seed(9305)).to("cuda")
+    k2 = torch.empty_like(d["k_pool"]).index_copy_(0, perm, d["k_pool"])
+    v2 = torch.empty_like(d["v_pool"]).index_copy_(0, perm, d["v_pool"])
+    bt = d["block_table"]
+    bt2 = torch.where(bt >= 0, perm[bt.clamp(min=0).long()].to(torch.int32), bt).contiguous()
+    o2, l2 = decode(pools=(k2, v2), table=bt2)
+    say("decode relabel: comparing bits")
+    assert torch.equal(bits(o1), bits(o2)) and torch.equal(bits(l1), bits(l2)), "decode changed under a relabelling"
+
+    host = w.block_table.copy()
+    used = set(host[host >= 0].tolist())
+    free = [i for i in range(w.num_blocks) if i not in used]
+    k3, v3 = d["k_pool"].clone(), d["v_pool"].clone()
+    for b in range(1, len(P)):
+        fresh = np.asarray(free[(b - 1) * sh:b * sh], dtype=np.int64)
+        src = torch.from_numpy(host[b, :sh].astype(np.int64)).to("cuda")
+        dst = torch.from_numpy(fresh).to("cuda")
+        k3.index_copy_(0, dst, d["k_pool"].index_select(0, src))
+        v3.index_copy_(0, dst, d["v_pool"].index_select(0, src))
+        host[b, :sh] = fresh
+    o3, l3 = decode(pools=(k3, v3), table=torch.from_numpy(host).to("cuda"))
+    say("decode fork sharing: comparing bits")
+    assert torch.equal(bits(o1), bits(o3)) and torch.equal(bits(l1), bits(l3)), "decode differs on private copies"
+    kp, vp = oracle_append(w.k_pool_c, w.v_pool_c, w.compact_table, w.prefix_len, w.suffix_len, w.k_new, w.v_new)
+    ref, ref_l = oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len, w.suffix_len, w.num_kv_heads, w.scale)
+    compare(to_f64(o1, w.dtype), ref, "decode vs oracle")
+    compare(l1.cpu().numpy().astype(np.float64), ref_l, "decode lse vs oracle")
