@@ -10,6 +10,10 @@ and a pool with spare pages, then checks:
   (workspace) and without them (no workspace);
 * cascade extend, for cases drawn with a shared prefix;
 * decode, for cases drawn with one new token per sequence.
+
+A second, wider set draws up to 12 sequences, prefixes up to 4000 positions,
+shared prefixes up to 119 pages and 1-24 query heads per kv-head (new tokens
+scaled so the oracle's work per case stays bounded).
 """
 import numpy as np
 import pytest
@@ -58,17 +62,52 @@ def draw(case: int) -> dict:
                 shared_blocks=sh, extra_pages=int(rng.integers(0, 300)))
 
 
+def draw_wide(case: int) -> dict:
+    rng = np.random.default_rng(20000 + case)
+    B = int(rng.integers(1, 13))
+    kind = ("decode" if case % 5 == 4 else "shared" if case % 5 == 2 else "plain")
+    hkv = int(rng.choice([1, 2, 4, 8]))
+    G = int(rng.choice([1, 2, 3, 5, 7, 8, 12, 16, 24]))
+    D = int(rng.choice([64, 128]))
+    dtype = "f32" if rng.random() < 0.2 else "bf16"
+    sh = 0
+    smax = max(2, 2400 // (B * G * hkv))
+    if kind == "decode":
+        P = rng.integers(0, 4000, B)
+        S = np.ones(B, dtype=np.int64)
+    elif kind == "shared":
+        sh = int(rng.integers(1, 120))
+        P = sh * 16 + rng.integers(0, 2500, B)
+        S = rng.integers(1, smax + 1, B)
+    else:
+        P = rng.integers(0, 4000, B)
+        S = rng.integers(1, smax + 1, B)
+    return dict(kind=kind, B=B, P=[int(x) for x in P], S=[int(x) for x in S], hkv=hkv, G=G, D=D, dtype=dtype,
+                shared_blocks=sh, extra_pages=int(rng.integers(0, 300)))
+
+
 CASES = [draw(c) for c in range(N_CASES)]
+N_WIDE = 100
+WIDE = [draw_wide(c) for c in range(N_WIDE)]
 
 
 @pytest.mark.timeout(300)
 @pytest.mark.parametrize("case", range(N_CASES))
 def test_random_shape(case):
-    c = CASES[case]
+    check(CASES[case], f"rand{case}", 9100 + case)
+
+
+@pytest.mark.timeout(300)
+@pytest.mark.parametrize("case", range(N_WIDE))
+def test_random_wide_shape(case):
+    check(WIDE[case], f"wide{case}", 21000 + case)
+
+
+def check(c, case, seed):
     say(f"random case {case}: {c}")
     L = np.asarray(c["P"]) + np.asarray(c["S"])
     pages = int(c["shared_blocks"] + ((L + 15) // 16 - c["shared_blocks"]).sum())
-    w = build_workload(name=f"rand{case}", seed=9100 + case, prefix_len=c["P"], suffix_len=c["S"],
+    w = build_workload(name=case, seed=seed, prefix_len=c["P"], suffix_len=c["S"],
                        num_q_heads=c["G"] * c["hkv"], num_kv_heads=c["hkv"], head_dim=c["D"], dtype=c["dtype"],
                        num_blocks=pages + c["extra_pages"], shared_prefix_blocks=c["shared_blocks"])
     d = stage(w)
@@ -87,21 +126,21 @@ def test_random_shape(case):
         out, lse = kvt.decode_attention(d["q"], d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.scale,
                                         return_lse=True, checked=True)
         torch.cuda.synchronize()
-        compare(to_f64(out, w.dtype), ref_o, f"rand{case} decode out")
-        compare(lse.cpu().numpy().astype(np.float64), ref_l, f"rand{case} decode lse")
+        compare(to_f64(out, w.dtype), ref_o, f"{case} decode out")
+        compare(lse.cpu().numpy().astype(np.float64), ref_l, f"{case} decode lse")
 
     for use_ws in (True, False):
         out, lse = kvt.extend_attention(*args, w.scale, return_lse=True, use_workspace=use_ws, checked=True)
         torch.cuda.synchronize()
         tag = "split plan" if use_ws else "unsplit"
-        compare(to_f64(out, w.dtype), ref_o, f"rand{case} extend ({tag}) out")
-        compare(lse.cpu().numpy().astype(np.float64), ref_l, f"rand{case} extend ({tag}) lse")
+        compare(to_f64(out, w.dtype), ref_o, f"{case} extend ({tag}) out")
+        compare(lse.cpu().numpy().astype(np.float64), ref_l, f"{case} extend ({tag}) lse")
 
     if c["kind"] == "shared":
         out, lse = kvt.cascade_extend_attention(*args, c["shared_blocks"] * 16, w.scale, return_lse=True,
                                                 checked=True)
         torch.cuda.synchronize()
-        compare(to_f64(out, w.dtype), ref_o, f"rand{case} cascade out")
-        compare(lse.cpu().numpy().astype(np.float64), ref_l, f"rand{case} cascade lse")
+        compare(to_f64(out, w.dtype), ref_o, f"{case} cascade out")
+        compare(lse.cpu().numpy().astype(np.float64), ref_l, f"{case} cascade lse")
     del d
     torch.cuda.empty_cache()
