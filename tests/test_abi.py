@@ -286,3 +286,15 @@ def test_binding_fails_loudly_without_the_library(monkeypatch):
     monkeypatch.setattr(kvt, "LIB_PATH", "/nonexistent/libkvt.so")
     with pytest.raises(RuntimeError, match="missing"):
         kvt.lib()
+
+
+def test_length_arrays_reject_values_outside_int32():
+    """The binding's host arrays: short lists of ints take a fast path, the
+    rest goes through numpy; neither wraps a value outside int32."""
+    assert list(kvt._i32_array([0, 5, 2 ** 31 - 1])) == [0, 5, 2 ** 31 - 1]
+    assert list(kvt._i32_array(np.array([[1, 2], [3, 4]]))) == [1, 2, 3, 4]
+    assert list(kvt._i32_array(list(range(100)))) == list(range(100))      # long list: numpy path
+    assert list(kvt._i32_array((np.int64(7), 8))) == [7, 8]                 # numpy scalars: numpy path
+    for bad in ([2 ** 31], [-2 ** 31 - 1], [1, 2 ** 40], list(range(99)) + [2 ** 33]):
+        with pytest.raises((OverflowError, ValueError)):
+            kvt._i32_array(bad)
