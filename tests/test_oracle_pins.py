@@ -125,6 +125,69 @@ def test_brute_force_catches_planted_mistakes():
 
 
 # ---------------------------------------------------------------------------
+# the oracle's own input decoding and row sampling
+# ---------------------------------------------------------------------------
+
+# bf16 bit pattern -> value, derived from the format (sign, 8 exponent bits with
+# bias 127, 7 fraction bits): 0x3F80 = +2^0; 0xC020 = -(1 + 1/4) * 2^1;
+# 0x0001 = the smallest subnormal 2^-126 * 2^-7; 0x0080 = the smallest normal
+# 2^-126; 0x7F7F = the largest finite (2 - 2^-7) * 2^127; 0x4049 =
+# (1 + 73/128) * 2^1; 0x3E80 = 2^-2; 0x7F80 / 0xFF80 = +-inf; 0x8000 = -0.
+BF16_PATTERNS = [
+    (0x3F80, 1.0), (0xC020, -2.5), (0x0001, 2.0 ** -133), (0x0080, 2.0 ** -126),
+    (0x7F7F, (2.0 - 2.0 ** -7) * 2.0 ** 127), (0x4049, 3.140625), (0x3E80, 0.25),
+    (0x7F80, math.inf), (0xFF80, -math.inf), (0x8000, -0.0), (0x0000, 0.0),
+]
+
+
+def test_bf16_storage_decodes_fixed_bit_patterns():
+    """Every CPU comparison on bf16 data widens both sides through
+    ``storage_to_f64``; pin its bf16 branch on hand-decoded bit patterns (a
+    shifted, sign-dropped or byte-swapped decoding fails here) and against
+    torch's own bfloat16 -> float64 conversion."""
+    torch = pytest.importorskip("torch")
+    bits = np.array([p for p, _ in BF16_PATTERNS], dtype=np.uint16)
+    got = storage_to_f64(bits)
+    assert got.dtype == np.float64
+    for (p, want), g in zip(BF16_PATTERNS, got):
+        assert g == want and math.copysign(1.0, g) == math.copysign(1.0, want), hex(p)
+    assert np.isnan(storage_to_f64(np.array([0x7FC0, 0xFFC1], dtype=np.uint16))).all()
+    # all 65536 patterns agree with torch's conversion (NaNs as NaNs)
+    every = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    with np.errstate(invalid="ignore"):          # widening NaN payloads
+        ours = storage_to_f64(every)
+    theirs = torch.from_numpy(every.view(np.int16)).view(torch.bfloat16).to(torch.float64).numpy()
+    nan = np.isnan(theirs)
+    assert np.array_equal(np.isnan(ours), nan)
+    assert np.array_equal(ours[~nan].view(np.uint64), theirs[~nan].view(np.uint64))
+    # float32 storage is widened unchanged
+    f = np.array([1.5, -0.0, 3.4e38, 1e-45], dtype=np.float32)
+    assert np.array_equal(storage_to_f64(f).view(np.uint64), f.astype(np.float64).view(np.uint64))
+
+
+def test_row_sampling_equals_brute_force_rows():
+    """``oracle_extend(rows=...)`` computes only the chosen suffix tokens; on a
+    ragged three-sequence batch (G = 12, chunks of two tokens so a selection
+    crosses several chunk boundaries, one sequence with no rows selected, one
+    with all) its rows equal brute force at those rows and the full call's."""
+    P, S = [37, 0, 120], [23, 9, 31]
+    w = build_workload(name="rows", seed=23, prefix_len=P, suffix_len=S, num_q_heads=24, num_kv_heads=2,
+                       head_dim=16, dtype="bf16", num_blocks=64, keep_logical=True)
+    kp, vp = _appended(w)
+    rows = [np.array([0, 3, 4, 5, 11, 21, 22]), np.array([], dtype=np.int64), None]
+    out, lse = oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len, w.suffix_len, 2, w.scale, rows=rows,
+                             chunk_rows=24)
+    assert out.shape == (7 + 0 + 31, 24, 16) and lse.shape == (38, 24)
+    bo, bl = brute_force_extend(w.q, w.logical_k, w.logical_v, w.prefix_len, w.suffix_len, 2, w.scale)
+    fo, fl = oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len, w.suffix_len, 2, w.scale)
+    off = w.seq_offsets
+    idx = np.concatenate([off[0] + rows[0], off[2] + np.arange(S[2])])
+    assert _rel(out, bo[idx]) <= 1e-12
+    assert np.max(np.abs(lse - bl[idx])) <= 1e-12 * np.max(np.abs(bl))
+    assert np.array_equal(out, fo[idx]) and np.array_equal(lse, fl[idx])
+
+
+# ---------------------------------------------------------------------------
 # library routines
 # ---------------------------------------------------------------------------
 
@@ -188,15 +251,37 @@ def test_constant_values_reproduce_the_constant():
 
 
 def test_needle_selects_its_target_value():
-    """q = 2 K[t] puts logit ~ 2 sqrt(D) on position t, far above the others,
-    so the output is V[t] up to the small residual mass (bounded here by 1e-2)."""
+    """A needle query puts logit ~40 on its target position t; every other
+    logit is N(0, 1600/|K_t|^2), so the output is V[t] up to a residual mass
+    of about e^-30 here, and lse sits at 40 up to the bf16 rounding of q."""
     w = build_workload(name="nd", seed=15, prefix_len=[2000], suffix_len=[8], num_q_heads=4, num_kv_heads=1,
                        head_dim=128, dtype="bf16", num_blocks=256, variant="needle", keep_logical=True)
-    out, _ = _oracle(w)
+    out, lse = _oracle(w)
     tgt = w.extra["needle_target"]
     v = storage_to_f64(w.logical_v[0])
     want = v[tgt, 0, :]                                          # [T, Hq, D]
-    assert np.max(np.abs(out - want)) < 1e-2
+    assert np.max(np.abs(out - want)) < 1e-9
+    assert np.max(np.abs(lse - 40.0)) < 0.5
+
+
+def test_needle_targets_cover_every_page():
+    """Per kv-head the latest (token, head) pairs point at distinct pages, so
+    when a sequence has at least as many pairs per kv-head as pages, every
+    page (the partly filled last one too) is a target of every kv-head, and
+    every target is a position its query may see."""
+    P, S = [130, 61], [40, 7]
+    w = build_workload(name="cov", seed=24, prefix_len=P, suffix_len=S, num_q_heads=6, num_kv_heads=2,
+                       head_dim=16, dtype="bf16", num_blocks=64, variant="needle")
+    tgt = w.extra["needle_target"]
+    off = w.seq_offsets
+    for b in range(2):
+        t = tgt[off[b]:off[b + 1]]
+        assert np.all(t >= 0) and np.all(t <= P[b] + np.arange(S[b])[:, None])
+        nblk = (P[b] + S[b] + 15) // 16
+        for g in range(2):
+            pages = set((t[:, 3 * g:3 * g + 3] // 16).reshape(-1).tolist())
+            if S[b] * 3 >= nblk:
+                assert pages == set(range(nblk))
 
 
 # ---------------------------------------------------------------------------
