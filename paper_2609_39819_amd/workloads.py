@@ -131,11 +131,18 @@ def _normal(rng: np.random.Generator, shape, dtype: str) -> np.ndarray:
     return x
 
 
-def _storage_scale2(x: np.ndarray, dtype: str) -> np.ndarray:
-    """Exact doubling of stored values (bf16: +1 on the exponent field via float32)."""
-    if dtype == "bf16":
-        return f32_to_bf16_bits(bf16_bits_to_f32(x) * np.float32(2.0))
-    return x * np.float32(2.0)
+# logit of a needle query's target position (natural-log units)
+NEEDLE_LOGIT = 40.0
+
+
+def _needle_query(keys: np.ndarray, dtype: str, scale: float) -> np.ndarray:
+    """Stored queries whose logit against their own target key is about
+    NEEDLE_LOGIT: q = NEEDLE_LOGIT / (scale * |k|^2) * k, rounded to storage."""
+    k = bf16_bits_to_f32(keys) if dtype == "bf16" else keys
+    k64 = k.astype(np.float64)
+    n2 = np.maximum((k64 * k64).sum(axis=-1, keepdims=True), 1e-30)
+    qv = (NEEDLE_LOGIT / (scale * n2) * k64).astype(np.float32)
+    return f32_to_bf16_bits(qv) if dtype == "bf16" else qv
 
 
 def build_workload(
@@ -165,8 +172,16 @@ def build_workload(
       * ``normal``  Q, K, V ~ N(0,1)
       * ``kzero``   every key is zero (logits all zero)
       * ``vconst``  every value row of kv-head g equals one vector c_g
-      * ``needle``  q[t,h] = 2 * K_b[target] with target uniform over the
-                    positions that query may see; stores ``extra["needle_target"]``
+      * ``needle``  q[t,h] = NEEDLE_LOGIT / (scale * |K_b[target]|^2) * K_b[target]
+                    (stored rounded), so the target's logit is NEEDLE_LOGIT
+                    whatever its key's norm and it outweighs every other
+                    visible position by a factor of about e^14 even at 262144
+                    positions; the target is uniform over the positions that
+                    query may see, except that for each kv-head the latest
+                    (token, head) pairs point at distinct pages, last page
+                    first, so every page of a sequence is some query's target
+                    when the sequence has at least as many pairs per kv-head
+                    as pages; stores ``extra["needle_target"]``
     """
     if rng is None:
         rng = np.random.default_rng(seed)
@@ -240,16 +255,30 @@ def build_workload(
     elif variant == "needle":
         # each (token, head) points at one visible key of its own sequence
         targets = np.empty((T, Hq), dtype=np.int64)
+        scale = 1.0 / math.sqrt(D)
         for b in range(B):
             t = np.arange(S[b])
             hi = P[b] + t  # inclusive upper bound of visible positions
             u = rng.random((S[b], Hq))
             tgt = np.minimum((u * (hi[:, None] + 1)).astype(np.int64), hi[:, None])
+            # page coverage: pair k of kv-head g in (latest token first, head)
+            # order targets page nblk-1-k; page 16*(nblk-1-k) <= P + token
+            # holds because the page index falls by one per pair and the
+            # token by one per G pairs
+            n_cov = int(min(nblk[b], S[b] * G))
+            k = np.arange(n_cov)
+            tok = S[b] - 1 - k // G
+            page = nblk[b] - 1 - k
+            slot_hi = np.minimum(BLOCK_SIZE - 1, P[b] + tok - BLOCK_SIZE * page)
+            for g in range(Hkv):
+                us = rng.random(n_cov)
+                slot = np.minimum((us * (slot_hi + 1)).astype(np.int64), slot_hi)
+                tgt[tok, g * G + k % G] = BLOCK_SIZE * page + slot
             targets[off[b]:off[b + 1]] = tgt
             kb = logical_k[b]
             for h in range(Hq):
                 g = h // G
-                q[off[b]:off[b + 1], h, :] = _storage_scale2(kb[tgt[:, h], g, :], dtype)
+                q[off[b]:off[b + 1], h, :] = _needle_query(kb[tgt[:, h], g, :], dtype, scale)
         extra["needle_target"] = targets
     elif variant != "normal":
         raise ValueError(f"unknown variant {variant!r}")
