@@ -144,7 +144,13 @@ def _i32_array(x) -> ctypes.Array:
     # outside int32 instead of wrapping them
     if type(x) in (list, tuple) and len(x) <= 64 and all(type(e) is int and _I32_MIN <= e <= _I32_MAX for e in x):
         return (ctypes.c_int32 * len(x))(*x)
-    a = np.ascontiguousarray(np.asarray(x, dtype=np.int32).reshape(-1))
+    a = np.asarray(x)
+    if a.dtype.kind not in "iu":
+        a = np.asarray(x, dtype=np.int64)          # raises on ints beyond int64
+    a = a.reshape(-1)
+    if a.size and (int(a.min()) < _I32_MIN or int(a.max()) > _I32_MAX):
+        raise OverflowError("length or block id outside the int32 range")
+    a = np.ascontiguousarray(a.astype(np.int32))
     return (ctypes.c_int32 * a.size).from_buffer_copy(a)
 
 
@@ -304,6 +310,14 @@ def decode_attention(q, k_pool, v_pool, block_table, prefix_len: Sequence[int], 
 def _attention(entry: str, ws_entry: str, q, k_pool, v_pool, block_table, prefix_len, suffix_len, scale, out, lse,
                return_lse, workspace, use_workspace, stream, checked, shared: Optional[int] = None):
     import torch
+    if stream is not None:
+        # buffers allocated here (out, lse, the split workspace) belong to the
+        # stream the kernels run on: torch's caching allocator then hands a
+        # freed workspace to the next allocation on that stream only, which is
+        # ordered after these kernels
+        with torch.cuda.stream(stream):
+            return _attention(entry, ws_entry, q, k_pool, v_pool, block_table, prefix_len, suffix_len, scale, out,
+                              lse, return_lse, workspace, use_workspace, None, checked, shared)
     lead = () if shared is None else (shared,)   # the cascade entry points take shared_len after seqs
     pool = _pool_struct(k_pool, v_pool)
     seqs = _seqs(prefix_len, suffix_len, block_table, checked)

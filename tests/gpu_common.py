@@ -14,6 +14,11 @@ from paper_2609_39819_amd.workloads import make_config, stage_on_device, torch_t
 # parity tolerance for bf16 inputs
 MAX_ABS = 2e-2
 MEAN_ABS = 2e-3
+# relative L2 bound beside the absolute ones: at 128K+ keys the outputs' own
+# scale (std ~ sqrt(e / n)) is close to MEAN_ABS, so an all-zero or
+# quarter-wrong output can sit inside the absolute bounds but not this one
+# (the kernels measure 2e-3 .. 4e-3: bf16 rounding of P and of the output)
+REL_L2 = 1e-2
 
 
 def say(*a):
@@ -87,7 +92,7 @@ def gather_rows(arr, w, rows):
     return arr[idx]
 
 
-def compare(got, want, label, max_abs=MAX_ABS, mean_abs=MEAN_ABS):
+def compare(got, want, label, max_abs=MAX_ABS, mean_abs=MEAN_ABS, rel_l2=REL_L2):
     diff = np.abs(got - want)
     ma, me = float(diff.max()), float(diff.mean())
     rel = float(np.linalg.norm(got - want) / max(1e-30, np.linalg.norm(want)))
@@ -95,4 +100,5 @@ def compare(got, want, label, max_abs=MAX_ABS, mean_abs=MEAN_ABS):
     assert np.all(np.isfinite(got)), f"{label}: non-finite output"
     assert ma <= max_abs, f"{label}: max_abs {ma} > {max_abs}"
     assert me <= mean_abs, f"{label}: mean_abs {me} > {mean_abs}"
+    assert rel <= rel_l2, f"{label}: rel_l2 {rel} > {rel_l2}"
     return ma, me, rel

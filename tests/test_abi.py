@@ -295,6 +295,10 @@ def test_length_arrays_reject_values_outside_int32():
     assert list(kvt._i32_array(np.array([[1, 2], [3, 4]]))) == [1, 2, 3, 4]
     assert list(kvt._i32_array(list(range(100)))) == list(range(100))      # long list: numpy path
     assert list(kvt._i32_array((np.int64(7), 8))) == [7, 8]                 # numpy scalars: numpy path
-    for bad in ([2 ** 31], [-2 ** 31 - 1], [1, 2 ** 40], list(range(99)) + [2 ** 33]):
+    assert list(kvt._i32_array(np.array([3, 2 ** 31 - 1], dtype=np.int64))) == [3, 2 ** 31 - 1]
+    assert list(kvt._i32_array(np.array([7], dtype=np.uint64))) == [7]
+    for bad in ([2 ** 31], [-2 ** 31 - 1], [1, 2 ** 40], list(range(99)) + [2 ** 33],
+                np.array([2 ** 33 + 5], dtype=np.int64), np.array([-2 ** 31 - 1], dtype=np.int64),
+                np.array([2 ** 32], dtype=np.uint64), [2 ** 70]):
         with pytest.raises((OverflowError, ValueError)):
             kvt._i32_array(bad)

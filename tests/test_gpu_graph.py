@@ -124,3 +124,34 @@ def test_extend_replays_from_a_graph_and_runs_on_two_streams():
     torch.cuda.synchronize()
     assert torch.equal(out.view(torch.int16), ref.view(torch.int16))
     assert torch.equal(out2.view(torch.int16), ref.view(torch.int16))
+
+
+@pytest.mark.timeout(300)
+def test_explicit_stream_owns_the_buffers_the_binding_allocates():
+    """``stream=`` for a stream other than the current one: the output, lse
+    and split workspace the binding allocates belong to that stream, so
+    allocations and writes on the current stream right after the call (before
+    any synchronisation) cannot land on the workspace the kernels still use."""
+    w = build_workload(name="stream_arg", seed=883, prefix_len=[8000, 6000], suffix_len=[64, 32], num_q_heads=16,
+                       num_kv_heads=4, head_dim=128, dtype="bf16", num_blocks=4096)
+    d = stage(w)
+    kvt.append_kv(d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.suffix_len, d["k_new"], d["v_new"])
+    need = kvt.extend_workspace_bytes(d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.suffix_len,
+                                      w.num_q_heads)
+    assert need > 0, "the call is split, so the binding allocates a workspace"
+    ref, ref_lse = kvt.extend_attention(d["q"], d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len,
+                                        w.suffix_len, w.scale, return_lse=True)
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    for r in range(3):
+        s.wait_stream(torch.cuda.current_stream())
+        out, lse = kvt.extend_attention(d["q"], d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len,
+                                        w.suffix_len, w.scale, return_lse=True, stream=s)
+        # the current stream allocates workspace-sized buffers and writes them at once
+        junk = [torch.empty(need, dtype=torch.uint8, device="cuda") for _ in range(4)]
+        for j in junk:
+            j.fill_(0x7F)
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), ref.view(torch.int16)), f"call {r}: out differs"
+        assert torch.equal(lse, ref_lse), f"call {r}: lse differs"
+        del junk, out, lse
