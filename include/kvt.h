@@ -28,7 +28,10 @@
  *   registers and take the same path.  Softmax and accumulation are fp32.
  * Ownership: every buffer belongs to the caller.  The library allocates no
  *   device memory and keeps no state between calls except a cached device
- *   property; calls are reentrant.
+ *   property and, for kvt_extend_attention_noalloc only, one static scratch
+ *   array per GPU (KVT_NOALLOC_SCRATCH_BYTES) and its looked-up address;
+ *   calls are reentrant, except that no-alloc calls overlapping on one GPU
+ *   share that scratch.
  * Asynchrony: KVT_OK means the work is enqueued on `stream` (a hipStream_t;
  *   NULL = the default stream).  Device-side faults surface at the caller's
  *   next synchronisation.  Pool pages read or written by a call must not be
@@ -59,7 +62,8 @@ typedef enum {
   KVT_ERR_UNSUPPORTED = 2,   /* head_dim not in {64,128}, unknown dtype */
   KVT_ERR_OUT_OF_RANGE = 3,  /* checked mode: block id outside [0,num_blocks) or duplicate append slot */
   KVT_ERR_WORKSPACE = 4,     /* non-null workspace smaller than kvt_extend_workspace_bytes() */
-  KVT_ERR_DEVICE = 5         /* HIP launch failure; see kvt_last_hip_error() */
+  KVT_ERR_DEVICE = 5,        /* HIP launch failure; see kvt_last_hip_error() */
+  KVT_ERR_SCRATCH_LIMIT = 6  /* kvt_extend_attention_noalloc: partials exceed KVT_NOALLOC_SCRATCH_BYTES */
 } kvt_status;
 
 typedef enum { KVT_DTYPE_BF16 = 0, KVT_DTYPE_F32 = 1 } kvt_dtype;
@@ -131,6 +135,32 @@ kvt_status kvt_extend_attention(const kvt_pool* pool, const kvt_seqs* seqs,
  * workgroups (short suffixes, small batches).  0 when no split is planned or
  * the arguments are invalid.  Host-only; enqueues nothing. */
 size_t kvt_extend_workspace_bytes(const kvt_pool* pool, const kvt_seqs* seqs, int32_t num_q_heads);
+
+/* Size of the static scratch array of kvt_extend_attention_noalloc (64 MiB),
+ * held by each GPU the library runs on until the process ends. */
+#define KVT_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/*
+ * kvt_extend_attention_noalloc -- kvt_extend_attention for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): no workspace argument, and no
+ * device allocation of any kind.
+ *
+ * Same arguments (less the workspace), checks and result as
+ * kvt_extend_attention with a workspace of kvt_extend_workspace_bytes(): the
+ * same split plan runs, so out and lse are bit-identical to that call.  The
+ * split partials go to a static array of KVT_NOALLOC_SCRATCH_BYTES that each
+ * GPU holds (looked up by its symbol address on the first call on that
+ * device).  A call whose plan needs more (kvt_extend_workspace_bytes() >
+ * KVT_NOALLOC_SCRATCH_BYTES) returns KVT_ERR_SCRATCH_LIMIT with nothing
+ * enqueued; an unsplit plan needs none.  Every call on one GPU shares that
+ * GPU's array, which keeps the last call's contents: two no-alloc calls that
+ * overlap on one GPU (different streams, no ordering between them) race and
+ * must not be issued; nothing in the array needs clearing between calls.
+ */
+kvt_status kvt_extend_attention_noalloc(const kvt_pool* pool, const kvt_seqs* seqs,
+                                        const void* q, int32_t num_q_heads, float scale,
+                                        void* out, float* lse, void* stream);
 
 /*
  * kvt_cascade_extend_attention -- kvt_extend_attention for a batch whose

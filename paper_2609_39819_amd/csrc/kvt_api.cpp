@@ -278,6 +278,49 @@ kvt_status combine(const kvt::ExtendArgs& a, const kvt_pool* pool, void* out, fl
   return e == hipSuccess ? KVT_OK : device_error(e);
 }
 
+// The argument checks of kvt_extend_attention (and its no-alloc variant);
+// fills the total token count.
+kvt_status check_extend(const kvt_pool* pool, const kvt_seqs* seqs, const void* q, int32_t num_q_heads, float scale,
+                        const void* out, const float* lse, int64_t* T) {
+  kvt_status st = check_pool(pool);
+  if (st != KVT_OK) return st;
+  if ((st = check_seqs(seqs, T)) != KVT_OK) return st;
+  if (q == nullptr || out == nullptr) return KVT_ERR_INVALID_ARG;
+  if (!heads_ok(pool, num_q_heads, *T)) return KVT_ERR_INVALID_ARG;
+  if (!(scale > 0.f) || !std::isfinite(scale)) return KVT_ERR_INVALID_ARG;
+  if ((st = check_table_ids(pool, seqs)) != KVT_OK) return st;
+  return check_outputs(pool, q, num_q_heads, out, lse, *T);
+}
+
+// Launches of one extend call under `plan` (partials in `workspace` when split).
+kvt_status launch_extend_plan(const kvt_pool* pool, const kvt_seqs* seqs, const void* q, int32_t num_q_heads,
+                              float scale, void* out, float* lse, int64_t T, const ExtendPlan& plan,
+                              void* workspace, void* stream) {
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const int G = num_q_heads / pool->num_kv_heads;
+  std::vector<int32_t> row_off(seqs->num_seqs + 1, 0);
+  for (int b = 0; b < seqs->num_seqs; ++b) row_off[b + 1] = row_off[b] + seqs->suffix_len[b];
+
+  kvt::ExtendArgs a = base_args(pool, seqs, q, num_q_heads, scale, out, lse, T, plan, workspace);
+  for (size_t c0 = 0; c0 < plan.order.size(); c0 += kvt::kSeqsPerLaunch) {
+    const int n = (int)std::min<size_t>(kvt::kSeqsPerLaunch, plan.order.size() - c0);
+    a.nseq = n;
+    int32_t units = 0;
+    for (int i = 0; i < n; ++i) {
+      const int b = plan.order[c0 + i];
+      a.seq[i] = kvt::SeqDesc{b, seqs->prefix_len[b], seqs->suffix_len[b], row_off[b]};
+      a.unit_begin[i] = units;
+      units += row_tiles(seqs->suffix_len[b], G) * plan.nsplit;
+    }
+    a.unit_begin[n] = units;
+    const int64_t grid = (int64_t)units * pool->num_kv_heads;
+    if (grid > INT32_MAX) return KVT_ERR_INVALID_ARG;
+    const hipError_t e = kvt::launch_extend(a, pool->dtype, pool->head_dim, (int)grid, s);
+    if (e != hipSuccess) return device_error(e);
+  }
+  return plan.nsplit > 1 ? combine(a, pool, out, lse, T, num_q_heads, plan.nsplit, s) : KVT_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -290,6 +333,7 @@ const char* kvt_status_str(kvt_status s) {
     case KVT_ERR_OUT_OF_RANGE: return "block id out of range or duplicate append target";
     case KVT_ERR_WORKSPACE: return "workspace too small";
     case KVT_ERR_DEVICE: return "HIP launch failed";
+    case KVT_ERR_SCRATCH_LIMIT: return "split partials exceed the static scratch (KVT_NOALLOC_SCRATCH_BYTES)";
   }
   return "unknown status";
 }
@@ -363,16 +407,9 @@ size_t kvt_extend_workspace_bytes(const kvt_pool* pool, const kvt_seqs* seqs, in
 kvt_status kvt_extend_attention(const kvt_pool* pool, const kvt_seqs* seqs, const void* q, int32_t num_q_heads,
                                 float scale, void* out, float* lse, void* workspace, size_t workspace_bytes,
                                 void* stream) {
-  kvt_status st = check_pool(pool);
-  if (st != KVT_OK) return st;
   int64_t T = 0;
-  if ((st = check_seqs(seqs, &T)) != KVT_OK) return st;
-  if (q == nullptr || out == nullptr) return KVT_ERR_INVALID_ARG;
-  if (!heads_ok(pool, num_q_heads, T)) return KVT_ERR_INVALID_ARG;
-  if (!(scale > 0.f) || !std::isfinite(scale)) return KVT_ERR_INVALID_ARG;
-  if ((st = check_table_ids(pool, seqs)) != KVT_OK) return st;
-  if ((st = check_outputs(pool, q, num_q_heads, out, lse, T)) != KVT_OK) return st;
-
+  const kvt_status st = check_extend(pool, seqs, q, num_q_heads, scale, out, lse, &T);
+  if (st != KVT_OK) return st;
   ExtendPlan plan = make_plan(pool, seqs, num_q_heads, T);
   if (plan.nsplit > 1) {
     if (workspace == nullptr && workspace_bytes == 0) {
@@ -383,30 +420,24 @@ kvt_status kvt_extend_attention(const kvt_pool* pool, const kvt_seqs* seqs, cons
       return KVT_ERR_INVALID_ARG;
     }
   }
+  return launch_extend_plan(pool, seqs, q, num_q_heads, scale, out, lse, T, plan, workspace, stream);
+}
 
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const int G = num_q_heads / pool->num_kv_heads;
-  std::vector<int32_t> row_off(seqs->num_seqs + 1, 0);
-  for (int b = 0; b < seqs->num_seqs; ++b) row_off[b + 1] = row_off[b] + seqs->suffix_len[b];
-
-  kvt::ExtendArgs a = base_args(pool, seqs, q, num_q_heads, scale, out, lse, T, plan, workspace);
-  for (size_t c0 = 0; c0 < plan.order.size(); c0 += kvt::kSeqsPerLaunch) {
-    const int n = (int)std::min<size_t>(kvt::kSeqsPerLaunch, plan.order.size() - c0);
-    a.nseq = n;
-    int32_t units = 0;
-    for (int i = 0; i < n; ++i) {
-      const int b = plan.order[c0 + i];
-      a.seq[i] = kvt::SeqDesc{b, seqs->prefix_len[b], seqs->suffix_len[b], row_off[b]};
-      a.unit_begin[i] = units;
-      units += row_tiles(seqs->suffix_len[b], G) * plan.nsplit;
-    }
-    a.unit_begin[n] = units;
-    const int64_t grid = (int64_t)units * pool->num_kv_heads;
-    if (grid > INT32_MAX) return KVT_ERR_INVALID_ARG;
-    const hipError_t e = kvt::launch_extend(a, pool->dtype, pool->head_dim, (int)grid, s);
+kvt_status kvt_extend_attention_noalloc(const kvt_pool* pool, const kvt_seqs* seqs, const void* q,
+                                        int32_t num_q_heads, float scale, void* out, float* lse, void* stream) {
+  int64_t T = 0;
+  const kvt_status st = check_extend(pool, seqs, q, num_q_heads, scale, out, lse, &T);
+  if (st != KVT_OK) return st;
+  // the same plan as kvt_extend_attention with a large enough workspace, so
+  // both give the same bits; partials go to the static scratch
+  const ExtendPlan plan = make_plan(pool, seqs, num_q_heads, T);
+  void* ws = nullptr;
+  if (plan.nsplit > 1) {
+    if (plan.ws_bytes > (size_t)KVT_NOALLOC_SCRATCH_BYTES) return KVT_ERR_SCRATCH_LIMIT;
+    const hipError_t e = kvt::noalloc_scratch(&ws);
     if (e != hipSuccess) return device_error(e);
   }
-  return plan.nsplit > 1 ? combine(a, pool, out, lse, T, num_q_heads, plan.nsplit, s) : KVT_OK;
+  return launch_extend_plan(pool, seqs, q, num_q_heads, scale, out, lse, T, plan, ws, stream);
 }
 
 kvt_status kvt_copy_blocks(const kvt_pool* pool, const int32_t* block_ids, const int32_t* block_ids_host,

@@ -101,5 +101,8 @@ hipError_t launch_combine(const CombineArgs& a, int dtype, int head_dim, hipStre
 hipError_t launch_copy_blocks(const CopyArgs& a, int grid, hipStream_t stream);
 // Decode: ExtendArgs with suffix 1 per sequence and nsplit units per sequence.
 hipError_t launch_decode(const ExtendArgs& a, int dtype, int head_dim, int grid, hipStream_t stream);
+// Device address of the current GPU's copy of the static scratch
+// (KVT_NOALLOC_SCRATCH_BYTES), looked up once per device.
+hipError_t noalloc_scratch(void** ptr);
 
 }  // namespace kvt

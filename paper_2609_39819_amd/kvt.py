@@ -23,6 +23,8 @@ KVT_ERR_UNSUPPORTED = 2
 KVT_ERR_OUT_OF_RANGE = 3
 KVT_ERR_WORKSPACE = 4
 KVT_ERR_DEVICE = 5
+KVT_ERR_SCRATCH_LIMIT = 6
+NOALLOC_SCRATCH_BYTES = 64 << 20    # KVT_NOALLOC_SCRATCH_BYTES
 KVT_DTYPE_BF16 = 0
 KVT_DTYPE_F32 = 1
 BLOCK_SIZE = 16
@@ -36,7 +38,8 @@ MGR_OPS = ("spawn", "fork", "append", "one_off", "pin", "unpin", "replace", "rem
            "start_prefill", "prefill_done", "end_request")   # KVT_MGR_OP_* in this order
 EXPORTED = ("kvt_append_kv", "kvt_cascade_extend_attention", "kvt_cascade_workspace_bytes", "kvt_copy_blocks",
             "kvt_decode_attention", "kvt_decode_workspace_bytes", "kvt_extend_attention",
-            "kvt_extend_workspace_bytes", "kvt_last_hip_error", "kvt_status_str") + MGR_EXPORTED
+            "kvt_extend_attention_noalloc", "kvt_extend_workspace_bytes", "kvt_last_hip_error",
+            "kvt_status_str") + MGR_EXPORTED
 KVT_COPY_TO_HOST = 0
 KVT_COPY_TO_DEVICE = 1
 KVT_PINNED, KVT_ACTIVE, KVT_SUSPENDED, KVT_EXPIRED, KVT_TEMPORARY = 0, 1, 2, 3, 4
@@ -87,6 +90,9 @@ def lib():
                                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                            ctypes.c_void_p]
         L.kvt_extend_attention.restype = ctypes.c_int
+        L.kvt_extend_attention_noalloc.argtypes = [P(KvtPool), P(KvtSeqs), ctypes.c_void_p, ctypes.c_int32,
+                                                   ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+        L.kvt_extend_attention_noalloc.restype = ctypes.c_int
         L.kvt_extend_workspace_bytes.argtypes = [P(KvtPool), P(KvtSeqs), ctypes.c_int32]
         L.kvt_extend_workspace_bytes.restype = ctypes.c_size_t
         L.kvt_cascade_extend_attention.argtypes = [P(KvtPool), P(KvtSeqs), ctypes.c_int32, ctypes.c_void_p,
@@ -244,6 +250,33 @@ def extend_attention(q, k_pool, v_pool, block_table, prefix_len: Sequence[int], 
     """
     return _attention("kvt_extend_attention", "kvt_extend_workspace_bytes", q, k_pool, v_pool, block_table,
                       prefix_len, suffix_len, scale, out, lse, return_lse, workspace, use_workspace, stream, checked)
+
+
+def extend_attention_noalloc(q, k_pool, v_pool, block_table, prefix_len: Sequence[int], suffix_len: Sequence[int],
+                             scale: Optional[float] = None, *, out, lse=None, stream=None, checked: bool = False):
+    """``kvt_extend_attention_noalloc``: the extend call with its split partials
+    in the library's static scratch; ``out`` (and ``lse`` if wanted) are the
+    caller's, so neither this function nor the library allocates device memory.
+    Raises ``KvtError`` (KVT_ERR_SCRATCH_LIMIT) when the split plan needs more
+    than ``NOALLOC_SCRATCH_BYTES``."""
+    pool = _pool_struct(k_pool, v_pool)
+    seqs = _seqs(prefix_len, suffix_len, block_table, checked)
+    T = sum(seqs.suffix)
+    Hq = int(q.shape[1])
+    _check_tokens(q, "q", T, Hq, pool.head_dim, k_pool.dtype)
+    _check_tokens(out, "out", T, Hq, pool.head_dim, k_pool.dtype)
+    if lse is not None and (str(lse.dtype) != "torch.float32" or tuple(lse.shape) != (T, Hq)
+                            or not lse.is_contiguous()):
+        raise ValueError("lse must be a contiguous float32 [T][Hq] tensor")
+    if scale is None:
+        scale = 1.0 / math.sqrt(pool.head_dim)
+    st = lib().kvt_extend_attention_noalloc(ctypes.byref(pool), ctypes.byref(seqs.struct), q.data_ptr(), Hq,
+                                            float(scale), out.data_ptr(),
+                                            lse.data_ptr() if lse is not None else None,
+                                            _stream_handle(q.device, stream))
+    if st != KVT_OK:
+        raise KvtError(st, "kvt_extend_attention_noalloc")
+    return out if lse is None else (out, lse)
 
 
 def cascade_workspace_bytes(k_pool, v_pool, block_table, prefix_len, suffix_len, shared_len: int,

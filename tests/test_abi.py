@@ -54,7 +54,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for code in range(6):
+    for code in range(7):
         assert kvt.status_str(code)
     assert kvt.status_str(99) == "unknown status"
     assert kvt.lib().kvt_last_hip_error() == 0
@@ -279,6 +279,28 @@ def test_small_workspace_is_rejected():
     pool = _pool(nb=65536, hkv=8, d=128)
     s = _seqs(P=(8192,), S=(512,), max_blocks=544)
     assert _extend(pool, s, hq=32, scale=0.088, ws=0x60000000000, ws_bytes=16) == kvt.KVT_ERR_WORKSPACE
+
+
+@no_gpu_only
+def test_noalloc_rejects_plans_beyond_its_static_scratch():
+    """kvt_extend_attention_noalloc runs the same split plan as
+    kvt_extend_attention; a plan whose partials exceed the static scratch is
+    refused on the host (one GPU's share of the 128K turn under 4-way head
+    parallelism: 4 key splits x 2048 x 24 rows x 130 floats = 102 MB)."""
+    pool = _pool(nb=1 << 20, hkv=2, d=128)
+    s = _seqs(P=(131072,), S=(2048,), max_blocks=8320)
+    need = _ws_bytes(pool, s, 24)
+    assert need > kvt.NOALLOC_SCRATCH_BYTES
+    L = kvt.lib()
+    st = L.kvt_extend_attention_noalloc(ctypes.byref(pool), ctypes.byref(s.struct), FAKE_Q, 24, 0.088, FAKE_OUT,
+                                        None, None)
+    assert st == kvt.KVT_ERR_SCRATCH_LIMIT
+    assert "scratch" in kvt.status_str(st)
+    # the same checks as the workspace entry point run first
+    assert L.kvt_extend_attention_noalloc(ctypes.byref(pool), ctypes.byref(s.struct), 0, 24, 0.088, FAKE_OUT,
+                                          None, None) == kvt.KVT_ERR_INVALID_ARG
+    assert L.kvt_extend_attention_noalloc(ctypes.byref(pool), ctypes.byref(s.struct), FAKE_Q, 25, 0.088, FAKE_OUT,
+                                          None, None) == kvt.KVT_ERR_INVALID_ARG
 
 
 def test_binding_fails_loudly_without_the_library(monkeypatch):
