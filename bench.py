@@ -230,6 +230,9 @@ def main():
     ap.add_argument("--cascade", action="store_true",
                     help="for a workload whose sequences share a prefix (forked_agents), run the cascade extend "
                          "(shared keys once for the whole batch, then the private keys, then an LSE merge)")
+    ap.add_argument("--cascade-mode", choices=("auto", "shared", "plain"), default="auto",
+                    help="with --cascade: let the library's estimate choose between the shared pass and the plain "
+                         "extend plan (auto, the default), or force one")
     ap.add_argument("--copy", action="store_true",
                     help="instead of attention, time moving every page of the workload to pinned host memory "
                          "and back (kvt_copy_blocks)")
@@ -295,8 +298,15 @@ def main():
     if decode:
         need = kvt.decode_workspace_bytes(d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, Hq)
     elif shared:
+        cmode = {"auto": kvt.CASCADE_AUTO, "shared": kvt.CASCADE_SHARED_PASS, "plain": kvt.CASCADE_PLAIN}[
+            args.cascade_mode]
         need = kvt.cascade_workspace_bytes(d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.suffix_len,
-                                           shared, Hq)
+                                           shared, Hq, mode=cmode)
+        cascade_plan = ("shared pass" if args.cascade_mode == "shared" else "plain" if args.cascade_mode == "plain"
+                        else "shared pass" if kvt.cascade_uses_shared_pass(d["k_pool"], d["v_pool"], d["block_table"],
+                                                                           w.prefix_len, w.suffix_len, shared, Hq)
+                        else "plain")
+        log(f"cascade mode {args.cascade_mode}: {cascade_plan}")
     else:
         need = kvt.extend_workspace_bytes(d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.suffix_len, Hq)
     ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev) if need else None
@@ -313,7 +323,8 @@ def main():
                                  out=out, workspace=ws, use_workspace=need > 0)
         elif shared:
             kvt.cascade_extend_attention(d["q"], d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len,
-                                         w.suffix_len, shared, w.scale, out=out, workspace=ws)
+                                         w.suffix_len, shared, w.scale, out=out, workspace=ws,
+                                         use_workspace=need > 0, mode=cmode)
         else:
             kvt.extend_attention(d["q"], d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.suffix_len,
                                  w.scale, out=out, workspace=ws, use_workspace=need > 0)
@@ -373,7 +384,8 @@ def main():
         },
         "new_tokens_per_s": w.total_tokens / (ms_per_step * 1e-3),
         "pct_bf16_peak": 100.0 * value / PEAK_BF16_TFLOPS,
-        "attention_kernel": "decode" if decode else ("cascade extend" if shared else "extend"),
+        "attention_kernel": "decode" if decode else (f"cascade extend ({args.cascade_mode}: {cascade_plan})"
+                                                     if shared else "extend"),
         "extend_ms": ext_avg,
         "extend_ms_median": float(np.median(ext_ms)),
         "extend_ms_min": float(ext_ms.min()),

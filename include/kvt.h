@@ -186,11 +186,36 @@ kvt_status kvt_cascade_extend_attention(const kvt_pool* pool, const kvt_seqs* se
                                         void* out, float* lse,
                                         void* workspace, size_t workspace_bytes, void* stream);
 
-/* Workspace of kvt_cascade_extend_attention: (1 + key splits of the private
- * parts) partial results per row.  0 when the arguments are invalid.
+/* Workspace of kvt_cascade_extend_attention: (key splits of the shared
+ * part + key splits of the private parts) partial results per row, or
+ * kvt_extend_workspace_bytes() when the call runs as the plain extend (see
+ * kvt_cascade_uses_shared_pass).  0 when the arguments are invalid.
  * Host-only; enqueues nothing. */
 size_t kvt_cascade_workspace_bytes(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shared_len,
                                    int32_t num_q_heads);
+
+/* Plan choice of the _ex cascade calls.  AUTO: the estimate below picks
+ * (what kvt_cascade_extend_attention and kvt_cascade_workspace_bytes do);
+ * SHARED_PASS: always the three-step cascade; PLAIN: always the plain extend
+ * plan.  Any other value gives KVT_ERR_INVALID_ARG (0 bytes). */
+typedef enum { KVT_CASCADE_AUTO = 0, KVT_CASCADE_SHARED_PASS = 1, KVT_CASCADE_PLAIN = 2 } kvt_cascade_mode;
+kvt_status kvt_cascade_extend_attention_ex(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shared_len,
+                                           int32_t mode, const void* q, int32_t num_q_heads, float scale,
+                                           void* out, float* lse,
+                                           void* workspace, size_t workspace_bytes, void* stream);
+size_t kvt_cascade_workspace_bytes_ex(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shared_len,
+                                      int32_t mode, int32_t num_q_heads);
+
+/* Whether kvt_cascade_extend_attention with a workspace runs the three-step
+ * cascade (1) or the plain extend plan (0), which it does when a host
+ * estimate (key tiles of work over the CUs plus the partial results the
+ * cascade writes and merges) says the plain extend is faster: with long
+ * suffixes every sequence's row tiles are nearly full, so the shared pass
+ * saves little key traffic and its partials cost more.  The result is the
+ * same either way; the plain plan gives the same bits as
+ * kvt_extend_attention.  -1 for invalid arguments.  Host-only. */
+int32_t kvt_cascade_uses_shared_pass(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shared_len,
+                                     int32_t num_q_heads);
 
 /*
  * kvt_decode_attention -- one decoding step: attention of each sequence's

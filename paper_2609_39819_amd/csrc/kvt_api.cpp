@@ -117,6 +117,7 @@ size_t part_bytes(const kvt_pool* pool, int nsplit, int64_t rows) {
 struct ExtendPlan {
   int nsplit = 1;
   int nsplit_shared = 0;    // cascade only: key splits of the shared part
+  bool use_shared = true;   // cascade only: false = run the plain extend plan
   std::vector<int> order;   // sequences, longest key range first
   size_t ws_bytes = 0;      // workspace needed for nsplit > 1
 };
@@ -197,14 +198,40 @@ kvt_status check_shared(const kvt_seqs* seqs, int32_t shared_len) {
   return KVT_OK;
 }
 
+// Estimated time of one extend launch in units of one 64-key tile of one
+// 256-row workgroup: the larger of the work spread over the CUs and the
+// longest unit's share of its key splits, plus the split partials written
+// and read back when split.  kt[b]: key tiles of sequence b, units[b]: its
+// row tiles x kv-heads.
+double launch_estimate(const std::vector<int64_t>& units, const std::vector<int64_t>& kt, int nsplit,
+                       int64_t rows, const kvt_pool* pool, int cus) {
+  // one tile of one workgroup takes about 1.8 us at full load; the partials
+  // move at about 5 bytes per ns (written once, read once by the combine)
+  constexpr double kTileUs = 1.8, kBytesPerUs = 5.0e6;
+  double work = 0, longest = 0;
+  for (size_t b = 0; b < units.size(); ++b) {
+    work += (double)units[b] * kt[b];
+    longest = std::max(longest, (double)kt[b]);
+  }
+  double t = std::max(work / cus, longest / nsplit);
+  if (nsplit > 1) t += 2.0 * (double)part_bytes(pool, nsplit, rows) / kBytesPerUs / kTileUs;
+  return t;
+}
+
 // Cascade: the split plans of the shared part (one virtual sequence of all T
 // new tokens over the shared keys, all visible) and of the private parts
 // (prefix lengths less the shared prefix); the workspace holds one partial
-// per split of either part.
+// per split of either part.  The shared pass reads the shared keys once per
+// packed row tile of the whole batch instead of once per sequence's row
+// tiles, but every row then goes through partials and a merge; when the
+// estimate says the plain extend is faster (long suffixes, where row tiles
+// pack well anyway), the plan is the plain extend's (use_shared = false).
 ExtendPlan cascade_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shared_len, int32_t num_q_heads,
-                        int64_t T) {
-  std::vector<int32_t> priv(seqs->num_seqs);
-  for (int b = 0; b < seqs->num_seqs; ++b) priv[b] = seqs->prefix_len[b] - shared_len;
+                        int64_t T, int32_t mode = KVT_CASCADE_AUTO) {
+  const int B = seqs->num_seqs, G = num_q_heads / pool->num_kv_heads, H = pool->num_kv_heads;
+  const int KT = kvt::kExtKeysPerTile;
+  std::vector<int32_t> priv(B);
+  for (int b = 0; b < B; ++b) priv[b] = seqs->prefix_len[b] - shared_len;
   kvt_seqs ps = *seqs;
   ps.prefix_len = priv.data();
   ExtendPlan p = make_plan(pool, &ps, num_q_heads, T);
@@ -215,7 +242,35 @@ ExtendPlan cascade_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shar
   ss.suffix_len = &all_tokens;
   p.nsplit_shared = make_plan(pool, &ss, num_q_heads, T).nsplit;
   p.ws_bytes = part_bytes(pool, p.nsplit_shared + p.nsplit, T * num_q_heads);
-  return p;
+  if (mode == KVT_CASCADE_SHARED_PASS) return p;
+
+  const ExtendPlan plain = make_plan(pool, seqs, num_q_heads, T);
+  if (mode == KVT_CASCADE_PLAIN) {
+    ExtendPlan q = plain;
+    q.use_shared = false;
+    return q;
+  }
+  const int cus = device_cus();
+  std::vector<int64_t> units(B), kt_full(B), kt_priv(B);
+  for (int b = 0; b < B; ++b) {
+    units[b] = (int64_t)row_tiles(seqs->suffix_len[b], G) * H;
+    kt_full[b] = ((int64_t)seqs->prefix_len[b] + seqs->suffix_len[b] + KT - 1) / KT;
+    kt_priv[b] = ((int64_t)priv[b] + seqs->suffix_len[b] + KT - 1) / KT;
+  }
+  const int64_t rows = T * num_q_heads;
+  const double t_plain = launch_estimate(units, kt_full, plain.nsplit, rows, pool, cus);
+  const double t_shared = launch_estimate({(int64_t)row_tiles((int32_t)T, G) * H}, {(shared_len + KT - 1) / KT},
+                                          p.nsplit_shared, 0, pool, cus) +
+                          launch_estimate(units, kt_priv, p.nsplit, 0, pool, cus) +
+                          2.0 * (double)p.ws_bytes / 5.0e6 / 1.8;
+  if (t_shared < t_plain) return p;
+  ExtendPlan q = plain;
+  q.use_shared = false;
+  return q;
+}
+
+bool mode_ok(int32_t mode) {
+  return mode == KVT_CASCADE_AUTO || mode == KVT_CASCADE_SHARED_PASS || mode == KVT_CASCADE_PLAIN;
 }
 
 // out must not overlap q or a pool; lse must not overlap out.
@@ -483,24 +538,47 @@ kvt_status kvt_copy_blocks(const kvt_pool* pool, const int32_t* block_ids, const
   return e == hipSuccess ? KVT_OK : device_error(e);
 }
 
-size_t kvt_cascade_workspace_bytes(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shared_len,
-                                   int32_t num_q_heads) {
+size_t kvt_cascade_workspace_bytes_ex(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shared_len,
+                                      int32_t mode, int32_t num_q_heads) {
   if (check_pool(pool) != KVT_OK) return 0;
   int64_t T = 0;
   if (check_seqs(seqs, &T) != KVT_OK) return 0;
   if (!heads_ok(pool, num_q_heads, T)) return 0;
-  if (check_shared(seqs, shared_len) != KVT_OK) return 0;
-  return cascade_plan(pool, seqs, shared_len, num_q_heads, T).ws_bytes;
+  if (check_shared(seqs, shared_len) != KVT_OK || !mode_ok(mode)) return 0;
+  return cascade_plan(pool, seqs, shared_len, num_q_heads, T, mode).ws_bytes;
+}
+
+size_t kvt_cascade_workspace_bytes(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shared_len,
+                                   int32_t num_q_heads) {
+  return kvt_cascade_workspace_bytes_ex(pool, seqs, shared_len, KVT_CASCADE_AUTO, num_q_heads);
+}
+
+int32_t kvt_cascade_uses_shared_pass(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shared_len,
+                                     int32_t num_q_heads) {
+  if (check_pool(pool) != KVT_OK) return -1;
+  int64_t T = 0;
+  if (check_seqs(seqs, &T) != KVT_OK) return -1;
+  if (!heads_ok(pool, num_q_heads, T)) return -1;
+  if (check_shared(seqs, shared_len) != KVT_OK) return -1;
+  return cascade_plan(pool, seqs, shared_len, num_q_heads, T).use_shared ? 1 : 0;
 }
 
 kvt_status kvt_cascade_extend_attention(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shared_len,
                                         const void* q, int32_t num_q_heads, float scale, void* out, float* lse,
                                         void* workspace, size_t workspace_bytes, void* stream) {
+  return kvt_cascade_extend_attention_ex(pool, seqs, shared_len, KVT_CASCADE_AUTO, q, num_q_heads, scale, out, lse,
+                                         workspace, workspace_bytes, stream);
+}
+
+kvt_status kvt_cascade_extend_attention_ex(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shared_len,
+                                           int32_t mode, const void* q, int32_t num_q_heads, float scale, void* out,
+                                           float* lse, void* workspace, size_t workspace_bytes, void* stream) {
   kvt_status st = check_pool(pool);
   if (st != KVT_OK) return st;
   int64_t T = 0;
   if ((st = check_seqs(seqs, &T)) != KVT_OK) return st;
   if ((st = check_shared(seqs, shared_len)) != KVT_OK) return st;
+  if (!mode_ok(mode)) return KVT_ERR_INVALID_ARG;
   if (workspace == nullptr && workspace_bytes == 0)   // no scratch: the plain extend computes the same
     return kvt_extend_attention(pool, seqs, q, num_q_heads, scale, out, lse, nullptr, 0, stream);
   if (q == nullptr || out == nullptr) return KVT_ERR_INVALID_ARG;
@@ -508,9 +586,11 @@ kvt_status kvt_cascade_extend_attention(const kvt_pool* pool, const kvt_seqs* se
   if (!(scale > 0.f) || !std::isfinite(scale)) return KVT_ERR_INVALID_ARG;
   if ((st = check_table_ids(pool, seqs)) != KVT_OK) return st;
   if ((st = check_outputs(pool, q, num_q_heads, out, lse, T)) != KVT_OK) return st;
-  const ExtendPlan plan = cascade_plan(pool, seqs, shared_len, num_q_heads, T);
+  const ExtendPlan plan = cascade_plan(pool, seqs, shared_len, num_q_heads, T, mode);
   if (workspace == nullptr || workspace_bytes < plan.ws_bytes) return KVT_ERR_WORKSPACE;
   if (!aligned16(workspace)) return KVT_ERR_INVALID_ARG;
+  if (!plan.use_shared)   // the plain extend is estimated faster: same result, same bits as kvt_extend_attention
+    return launch_extend_plan(pool, seqs, q, num_q_heads, scale, out, lse, T, plan, workspace, stream);
 
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const int G = num_q_heads / pool->num_kv_heads;

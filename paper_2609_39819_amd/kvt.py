@@ -36,10 +36,13 @@ MGR_EXPORTED = ("kvt_mgr_append", "kvt_mgr_begin_request", "kvt_mgr_create", "kv
                 "kvt_mgr_start_prefill", "kvt_mgr_terminate", "kvt_mgr_unpin")
 MGR_OPS = ("spawn", "fork", "append", "one_off", "pin", "unpin", "replace", "remove", "terminate", "begin_request",
            "start_prefill", "prefill_done", "end_request")   # KVT_MGR_OP_* in this order
-EXPORTED = ("kvt_append_kv", "kvt_cascade_extend_attention", "kvt_cascade_workspace_bytes", "kvt_copy_blocks",
+EXPORTED = ("kvt_append_kv", "kvt_cascade_extend_attention", "kvt_cascade_extend_attention_ex",
+            "kvt_cascade_uses_shared_pass", "kvt_cascade_workspace_bytes", "kvt_cascade_workspace_bytes_ex",
+            "kvt_copy_blocks",
             "kvt_decode_attention", "kvt_decode_workspace_bytes", "kvt_extend_attention",
             "kvt_extend_attention_noalloc", "kvt_extend_workspace_bytes", "kvt_last_hip_error",
             "kvt_status_str") + MGR_EXPORTED
+CASCADE_AUTO, CASCADE_SHARED_PASS, CASCADE_PLAIN = 0, 1, 2    # kvt_cascade_mode
 KVT_COPY_TO_HOST = 0
 KVT_COPY_TO_DEVICE = 1
 KVT_PINNED, KVT_ACTIVE, KVT_SUSPENDED, KVT_EXPIRED, KVT_TEMPORARY = 0, 1, 2, 3, 4
@@ -101,6 +104,16 @@ def lib():
         L.kvt_cascade_extend_attention.restype = ctypes.c_int
         L.kvt_cascade_workspace_bytes.argtypes = [P(KvtPool), P(KvtSeqs), ctypes.c_int32, ctypes.c_int32]
         L.kvt_cascade_workspace_bytes.restype = ctypes.c_size_t
+        L.kvt_cascade_uses_shared_pass.argtypes = L.kvt_cascade_workspace_bytes.argtypes
+        L.kvt_cascade_uses_shared_pass.restype = ctypes.c_int32
+        L.kvt_cascade_extend_attention_ex.argtypes = [P(KvtPool), P(KvtSeqs), ctypes.c_int32, ctypes.c_int32,
+                                                      ctypes.c_void_p, ctypes.c_int32, ctypes.c_float,
+                                                      ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                                      ctypes.c_size_t, ctypes.c_void_p]
+        L.kvt_cascade_extend_attention_ex.restype = ctypes.c_int
+        L.kvt_cascade_workspace_bytes_ex.argtypes = [P(KvtPool), P(KvtSeqs), ctypes.c_int32, ctypes.c_int32,
+                                                     ctypes.c_int32]
+        L.kvt_cascade_workspace_bytes_ex.restype = ctypes.c_size_t
         L.kvt_copy_blocks.argtypes = [P(KvtPool), ctypes.c_void_p, ctypes.POINTER(ctypes.c_int32), ctypes.c_int64,
                                       ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p]
         L.kvt_copy_blocks.restype = ctypes.c_int
@@ -280,22 +293,37 @@ def extend_attention_noalloc(q, k_pool, v_pool, block_table, prefix_len: Sequenc
 
 
 def cascade_workspace_bytes(k_pool, v_pool, block_table, prefix_len, suffix_len, shared_len: int,
-                            num_q_heads: int) -> int:
+                            num_q_heads: int, mode: int = CASCADE_AUTO) -> int:
     pool = _pool_struct(k_pool, v_pool)
     seqs = _seqs(prefix_len, suffix_len, block_table, False)
-    return int(lib().kvt_cascade_workspace_bytes(ctypes.byref(pool), ctypes.byref(seqs.struct), int(shared_len),
-                                                 int(num_q_heads)))
+    return int(lib().kvt_cascade_workspace_bytes_ex(ctypes.byref(pool), ctypes.byref(seqs.struct), int(shared_len),
+                                                    int(mode), int(num_q_heads)))
+
+
+def cascade_uses_shared_pass(k_pool, v_pool, block_table, prefix_len, suffix_len, shared_len: int,
+                             num_q_heads: int) -> bool:
+    """Whether ``cascade_extend_attention`` (with a workspace) runs the shared
+    pass or the plain extend plan (``kvt_cascade_uses_shared_pass``)."""
+    pool = _pool_struct(k_pool, v_pool)
+    seqs = _seqs(prefix_len, suffix_len, block_table, False)
+    r = int(lib().kvt_cascade_uses_shared_pass(ctypes.byref(pool), ctypes.byref(seqs.struct), int(shared_len),
+                                               int(num_q_heads)))
+    if r < 0:
+        raise ValueError("invalid cascade arguments")
+    return r == 1
 
 
 def cascade_extend_attention(q, k_pool, v_pool, block_table, prefix_len, suffix_len, shared_len: int,
                              scale: Optional[float] = None, *, out=None, lse=None, return_lse: bool = False,
-                             workspace=None, use_workspace: bool = True, stream=None, checked: bool = False):
+                             workspace=None, use_workspace: bool = True, stream=None, checked: bool = False,
+                             mode: int = CASCADE_AUTO):
     """Extend attention for sequences that share their first ``shared_len``
-    positions (``kvt_cascade_extend_attention``); same result as
-    ``extend_attention``."""
-    return _attention("kvt_cascade_extend_attention", "kvt_cascade_workspace_bytes", q, k_pool, v_pool,
+    positions (``kvt_cascade_extend_attention_ex``); same result as
+    ``extend_attention``.  ``mode``: CASCADE_AUTO (the library's estimate
+    picks the shared pass or the plain plan), CASCADE_SHARED_PASS, CASCADE_PLAIN."""
+    return _attention("kvt_cascade_extend_attention_ex", "kvt_cascade_workspace_bytes_ex", q, k_pool, v_pool,
                       block_table, prefix_len, suffix_len, scale, out, lse, return_lse, workspace, use_workspace,
-                      stream, checked, shared=int(shared_len))
+                      stream, checked, shared=(int(shared_len), int(mode)))
 
 
 def copy_blocks(k_pool, v_pool, block_ids, host, to_host: bool, *, stream=None, checked: bool = False):
@@ -351,7 +379,7 @@ def _attention(entry: str, ws_entry: str, q, k_pool, v_pool, block_table, prefix
         with torch.cuda.stream(stream):
             return _attention(entry, ws_entry, q, k_pool, v_pool, block_table, prefix_len, suffix_len, scale, out,
                               lse, return_lse, workspace, use_workspace, None, checked, shared)
-    lead = () if shared is None else (shared,)   # the cascade entry points take shared_len after seqs
+    lead = () if shared is None else shared     # the cascade entry points take (shared_len, mode) after seqs
     pool = _pool_struct(k_pool, v_pool)
     seqs = _seqs(prefix_len, suffix_len, block_table, checked)
     T = sum(seqs.suffix)

@@ -175,7 +175,11 @@ def test_cascade_specific_checks():
     host = np.stack([np.arange(16), np.arange(16, 32)]).astype(np.int32)   # first pages differ
     assert _cascade(_pool(), _seqs(P=(240, 100), S=(16, 16), max_blocks=16, host=host), 64,
                     ws=0x60000000000, ws_bytes=1 << 30) == E
-    assert _cascade(_pool(), two, 64, ws=0x60000000000, ws_bytes=16) == kvt.KVT_ERR_WORKSPACE
+    # a call that takes the shared pass (short messages over a long shared prefix) needs its partials
+    pool = _pool(nb=1 << 20, hkv=8, d=128)
+    short = _seqs(P=[32768 + 37 * i for i in range(16)], S=[16] * 16, max_blocks=2100)
+    assert kvt.lib().kvt_cascade_uses_shared_pass(ctypes.byref(pool), ctypes.byref(short.struct), 32768, 96) == 1
+    assert _cascade(pool, short, 32768, hq=96, ws=0x60000000000, ws_bytes=16) == kvt.KVT_ERR_WORKSPACE
 
 
 def test_cascade_workspace_bytes():
@@ -186,6 +190,24 @@ def test_cascade_workspace_bytes():
     parts = ws // (rows * (128 + 2) * 4)       # key splits of the shared part + of the private parts
     assert parts >= 2 and ws == -(-parts * rows * 128 * 4 // 256) * 256 + parts * rows * 2 * 4
     assert kvt.lib().kvt_cascade_workspace_bytes(ctypes.byref(pool), ctypes.byref(s.struct), 4100, 96) == 0
+
+
+def test_cascade_runs_the_plain_plan_when_its_estimate_loses():
+    """Short messages over a long shared prefix take the shared pass; long
+    suffixes (the forked-agents shape: every sequence's row tiles nearly full)
+    take the plain extend plan, whose workspace the call then asks for."""
+    L = kvt.lib()
+    pool = _pool(nb=1 << 20, hkv=8, d=128)
+    P = [32768 + 37 * i for i in range(16)]
+    short = _seqs(P=P, S=[16] * 16, max_blocks=2100)
+    assert L.kvt_cascade_uses_shared_pass(ctypes.byref(pool), ctypes.byref(short.struct), 32768, 96) == 1
+    P = [4096 + 3000 * i for i in range(16)]
+    S = [256 + 250 * i for i in range(16)]
+    long_ = _seqs(P=P, S=S, max_blocks=5000)
+    assert L.kvt_cascade_uses_shared_pass(ctypes.byref(pool), ctypes.byref(long_.struct), 4096, 96) == 0
+    assert (L.kvt_cascade_workspace_bytes(ctypes.byref(pool), ctypes.byref(long_.struct), 4096, 96)
+            == L.kvt_extend_workspace_bytes(ctypes.byref(pool), ctypes.byref(long_.struct), 96))
+    assert L.kvt_cascade_uses_shared_pass(ctypes.byref(pool), ctypes.byref(long_.struct), 4100, 96) == -1
 
 
 def _copy(pool, ids=FAKE_BT, ids_host=None, n=4, host=FAKE_OUT, direction=0):

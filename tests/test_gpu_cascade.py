@@ -1,13 +1,16 @@
-"""Cascade extend (``kvt_cascade_extend_attention``) against the fp64 oracle.
+"""Cascade extend (``kvt_cascade_extend_attention[_ex]``) against the fp64 oracle.
 
 The cascade computes the same attention as extend (shared keys for the whole
 batch at once, private keys per sequence, log-sum-exp merge), so the
-reference is ``oracle_extend``.  Covered: the forked-agents workload (4096
-shared positions, 16 sequences; sampled rows, lse, agreement with the plain
-extend kernel), short new messages over a 32768-position shared prefix, and
-edge shapes: a shared length that is not a multiple of the
-64-key tile, a sequence whose whole prefix is shared, a single sequence,
-D = 64, fp32 storage, and key splits in the private parts.
+reference is ``oracle_extend``.  In its default mode the call runs the plain
+extend plan whenever the library's estimate says the shared pass loses; the
+tests check that choice where it is clear-cut (the forked-agents workload:
+plain, bit-identical to ``kvt_extend_attention``; short messages over a long
+shared prefix: the shared pass) and force the shared pass on the
+forked-agents workload and on edge shapes (a shared length that is not a
+multiple of the 64-key tile, a sequence whose whole prefix is shared, a
+single sequence, D = 64, fp32 storage, key splits in the private parts),
+which are too small for it to win on its own.
 """
 import numpy as np
 import pytest
@@ -40,13 +43,35 @@ def run_cascade(w, d, shared, **kw):
     return r
 
 
+def uses_shared(w, d, shared):
+    return kvt.cascade_uses_shared_pass(d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.suffix_len,
+                                        shared, w.num_q_heads)
+
+
 @pytest.mark.timeout(900)
-def test_forked_agents_cascade_matches_oracle():
+def test_forked_agents_default_runs_the_plain_plan():
+    """Long suffixes: the estimate picks the plain extend plan, so the cascade
+    call gives exactly the bits of kvt_extend_attention."""
     w = cached_config("forked_agents")
     shared = config_shapes("forked_agents")["shared_prefix"]
     d = stage(w)
     run_append(w, d)
+    assert not uses_shared(w, d, shared)
     out, lse = run_cascade(w, d, shared, return_lse=True)
+    plain, plain_lse = run_extend(w, d, return_lse=True)
+    assert torch.equal(out.view(torch.int16), plain.view(torch.int16))
+    assert torch.equal(lse, plain_lse)
+    del d
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(900)
+def test_forked_agents_shared_pass_matches_oracle():
+    w = cached_config("forked_agents")
+    shared = config_shapes("forked_agents")["shared_prefix"]
+    d = stage(w)
+    run_append(w, d)
+    out, lse = run_cascade(w, d, shared, return_lse=True, mode=kvt.CASCADE_SHARED_PASS)
     rows = sample_rows(w, 6)
     kp, vp = oracle_pools("forked_agents")
     ref_o, ref_l = oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len, w.suffix_len, w.num_kv_heads, w.scale,
@@ -68,6 +93,7 @@ def test_short_messages_over_a_long_shared_prefix():
     shared = config_shapes("forked_short")["shared_prefix"]
     d = stage(w)
     run_append(w, d)
+    assert uses_shared(w, d, shared), "short messages over a long shared prefix take the shared pass by default"
     out, lse = run_cascade(w, d, shared, return_lse=True)
     rows = sample_rows(w, 8)
     kp, vp = oracle_pools("forked_short")
@@ -100,10 +126,16 @@ def test_cascade_edge_shapes(case):
                        num_kv_heads=Hkv, head_dim=D, dtype=dt, num_blocks=16384, shared_prefix_blocks=shared // 16)
     d = stage(w)
     run_append(w, d, checked=True)
-    out, lse = run_cascade(w, d, shared, return_lse=True, checked=True)
+    out, lse = run_cascade(w, d, shared, return_lse=True, checked=True, mode=kvt.CASCADE_SHARED_PASS)
     kp, vp = oracle_append(w.k_pool_c, w.v_pool_c, w.compact_table, w.prefix_len, w.suffix_len, w.k_new, w.v_new)
     ref_o, ref_l = oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len, w.suffix_len, Hkv, w.scale)
     compare(to_f64(out, dt), ref_o, f"casc_edge{case} out")
     compare(lse.cpu().numpy().astype(np.float64), ref_l, f"casc_edge{case} lse")
+    # the default mode: these shapes are too small for the shared pass to pay, so the plain plan runs
+    assert not uses_shared(w, d, shared)
+    auto = run_cascade(w, d, shared, checked=True)
+    plain = run_extend(w, d, checked=True)
+    assert torch.equal(auto.view(torch.int16 if dt == "bf16" else torch.int32),
+                       plain.view(torch.int16 if dt == "bf16" else torch.int32))
     del d
     torch.cuda.empty_cache()

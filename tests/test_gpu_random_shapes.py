@@ -138,6 +138,7 @@ def check(c, case, seed):
 
     if c["kind"] == "shared":
         out, lse = kvt.cascade_extend_attention(*args, c["shared_blocks"] * 16, w.scale, return_lse=True,
+                                                mode=kvt.CASCADE_SHARED_PASS,
                                                 checked=True)
         torch.cuda.synchronize()
         compare(to_f64(out, w.dtype), ref_o, f"{case} cascade out")
