@@ -58,8 +58,7 @@ __global__ __launch_bounds__(kWaves * 64) void decode_kernel(const ExtendArgs a)
   const int hkv = a.num_kv_heads;
   const int g = blockIdx.x % hkv;
   const int unit = blockIdx.x / hkv;
-  int si = 0;
-  while (si + 1 < a.nseq && a.unit_begin[si + 1] <= unit) ++si;
+  const int si = find_seq(a.unit_begin, a.nseq, unit);
   const SeqDesc sd = a.seq[si];
   const int split = unit - a.unit_begin[si];
   const int G = a.group;

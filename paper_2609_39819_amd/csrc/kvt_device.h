@@ -89,5 +89,18 @@ __device__ __forceinline__ float pair_sum(float x) {
   return a + b;
 }
 
+// Index of the sequence whose units contain `unit`: the last s < nseq with
+// begin[s] <= unit (begin ascending, begin[0] = 0), by binary search over
+// wave-uniform kernel arguments (at most 8 steps for 256 sequences).
+__device__ __forceinline__ int find_seq(const int32_t* begin, int nseq, int unit) {
+  int lo = 0, hi = nseq - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (begin[mid] <= unit) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
 }  // namespace dev
 }  // namespace kvt

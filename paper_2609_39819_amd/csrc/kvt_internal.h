@@ -11,7 +11,7 @@
 namespace kvt {
 
 constexpr int kBlock = 16;          // tokens per cache page
-constexpr int kSeqsPerLaunch = 64;  // sequences described by one launch
+constexpr int kSeqsPerLaunch = 256;  // sequences described by one launch (about 5.2 KiB of kernel arguments)
 
 // Extend tiling: one workgroup = 8 waves x 32 packed query rows, 64-key tiles.
 constexpr int kExtWaves = 8;
@@ -73,6 +73,9 @@ struct ExtendArgs {
   int32_t unit_begin[kSeqsPerLaunch + 1];  // prefix sums of (row tiles x nsplit), longest first
   SeqDesc seq[kSeqsPerLaunch];
 };
+
+// Launch arguments travel by value; larger batches take several launches.
+static_assert(sizeof(ExtendArgs) <= 8192 && sizeof(AppendArgs) <= 8192, "kernel argument block too large");
 
 struct CombineArgs {
   const float* part_o;

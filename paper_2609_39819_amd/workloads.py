@@ -319,9 +319,10 @@ def build_workload(
 CONFIG_NAMES = ("tiny", "gqa_8k", "react_128k", "forked_agents", "mutation_258k")
 # one GPU's share of the 128K turn under 4-way tensor parallelism (heads split
 # with no communication: 24 query heads over 2 kv-heads per GPU)
-# one decoding step of a batch of 32 agent contexts (one new token each)
+# one decoding step of a batch of 32 agent contexts (one new token each), and
+# of 256 contexts (a serving batch: one launch of 256 sequence descriptors)
 # 16 forked sub-agents each adding a short message over a long shared context
-EXTRA_CONFIG_NAMES = ("react_128k_tp4", "decode_batch", "forked_short")
+EXTRA_CONFIG_NAMES = ("react_128k_tp4", "decode_batch", "decode_batch256", "forked_short")
 
 
 def config_shapes(name: str) -> dict:
@@ -341,6 +342,9 @@ def config_shapes(name: str) -> dict:
     if name == "decode_batch":
         return dict(seed=7, num_q_heads=96, num_kv_heads=8, head_dim=128, dtype="bf16",
                     num_blocks=1 << 20, num_seqs=32, prefix=(2048, 32768), suffix=1)
+    if name == "decode_batch256":
+        return dict(seed=10, num_q_heads=96, num_kv_heads=8, head_dim=128, dtype="bf16",
+                    num_blocks=1 << 18, num_seqs=256, prefix=(1024, 8192), suffix=1)
     if name == "forked_agents":
         return dict(seed=4, num_q_heads=96, num_kv_heads=8, head_dim=128, dtype="bf16",
                     num_blocks=1 << 20, num_seqs=16, shared_prefix=4096,
@@ -372,7 +376,7 @@ def make_config(name: str, variant: str = "normal", keep_logical: Optional[bool]
     if name in ("forked_agents", "forked_short"):
         P, S = forked_lengths(rng, c["num_seqs"], c["shared_prefix"], c["private_prefix"], c["suffix"])
         sh_blocks = c["shared_prefix"] // BLOCK_SIZE
-    elif name == "decode_batch":
+    elif name in ("decode_batch", "decode_batch256"):
         # reused context lengths uniform over the inclusive range, one new token each
         P = rng.integers(c["prefix"][0], c["prefix"][1], size=c["num_seqs"], endpoint=True)
         S = np.ones(c["num_seqs"], dtype=np.int64)

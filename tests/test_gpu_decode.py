@@ -3,10 +3,12 @@
 One new token per sequence is the suffix-of-one case of extend attention, so
 the reference is ``oracle_extend`` with S_b = 1 on the pools ``oracle_append``
 produced.  Covered: the 32-sequence decode batch (all rows, lse, split and
-unsplit, run-to-run bit identity, agreement with the extend kernel), needle
-queries, and edge shapes (a single key, page and tile boundaries, the largest
-and smallest query groups, D = 64, fp32 storage, more sequences than one
-launch holds, one long sequence split 16 ways).
+unsplit, run-to-run bit identity, agreement with the extend kernel), the
+256-sequence batch (one launch: sampled sequences against the oracle, every
+row of a needle batch against its target value), needle queries, and edge
+shapes (a single key, page and tile boundaries, the largest and smallest
+query groups, D = 64, fp32 storage, more sequences than one launch holds,
+one long sequence split 16 ways).
 """
 import numpy as np
 import pytest
@@ -58,6 +60,38 @@ def test_decode_batch_matches_oracle():
     torch.cuda.empty_cache()
 
 
+@pytest.mark.timeout(900)
+def test_decode_batch256_in_one_launch():
+    """256 sequences fit one launch's descriptors.  On the needle variant of
+    the 256-sequence batch: 32 sampled sequences (every query head, out and
+    lse) against the oracle, and every row against the value at its target
+    position (a closed form that needs no oracle)."""
+    from oracle import gather_logical
+    w = cached_config("decode_batch256", "needle")
+    d = stage(w)
+    run_append(w, d)
+    out, lse = run_decode(w, d, return_lse=True)
+    got = to_f64(out, w.dtype)                                   # [256, Hq, D]
+    kp, vp = oracle_pools("decode_batch256", "needle")
+    pick = np.sort(np.random.default_rng(256).choice(w.num_seqs, 32, replace=False))
+    chosen = set(pick.tolist())
+    rows = [np.arange(1) if b in chosen else np.arange(0) for b in range(w.num_seqs)]
+    ref_o, ref_l = oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len, w.suffix_len, w.num_kv_heads, w.scale,
+                                 rows=rows)
+    compare(got[pick], ref_o, "decode_batch256 out (32 sequences)")
+    compare(lse.cpu().numpy().astype(np.float64)[pick], ref_l, "decode_batch256 lse (32 sequences)")
+    tgt, G = w.extra["needle_target"], w.group
+    want = np.empty_like(got)
+    for b in range(w.num_seqs):
+        L = int(w.prefix_len[b]) + 1
+        for g in range(w.num_kv_heads):
+            v = gather_logical(vp, w.compact_table[b], L, g)
+            want[b, g * G:(g + 1) * G] = v[tgt[b, g * G:(g + 1) * G]]
+    compare(got, want, "decode_batch256 needle vs V[target] (every row)")
+    del d
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.timeout(600)
 def test_decode_needle_finds_every_page():
     """q = 2 K[t] for a random earlier position t: out ~ V[t], so a wrong page,
@@ -84,9 +118,10 @@ DEC_EDGE = [
     ([1000, 5, 2047], 32, 1, 128, "bf16"),                     # G = 32, the largest group
     ([300, 4097], 8, 8, 128, "bf16"),                          # G = 1
     ([4000, 100], 8, 2, 64, "f32"),                            # fp32 storage, D = 64
-    (_rng.integers(0, 3000, size=70).tolist(), 12, 1, 128, "bf16"),   # two launches of sequences
+    (_rng.integers(0, 3000, size=70).tolist(), 12, 1, 128, "bf16"),   # 70 sequences, one launch
     ([20000], 12, 1, 128, "bf16"),                             # one sequence split 16 ways
     ([3, 9000, 64], 24, 2, 64, "bf16"),                        # D = 64, ragged
+    (_rng.integers(0, 400, size=300).tolist(), 8, 2, 64, "bf16"),   # 300 sequences: two launches
 ]
 
 

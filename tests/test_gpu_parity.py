@@ -179,8 +179,10 @@ EDGE = [
     ([15821], [1000], 1, 1, 128, "bf16"),
     ([300, 4100], [40, 17], 64, 2, 128, "bf16"),     # G = 32: a row tile holds 8 tokens
     ([2000], [33], 96, 1, 128, "bf16"),              # G = 96: one kv-head for all query heads
-    # 70 sequences: more than one launch's worth of sequence descriptors
+    # 70 sequences in one launch
     (_edge_rng.integers(0, 600, size=70).tolist(), _edge_rng.integers(1, 41, size=70).tolist(), 8, 2, 64, "bf16"),
+    # 300 sequences: more than one launch's worth (256) of sequence descriptors
+    (_edge_rng.integers(0, 300, size=300).tolist(), _edge_rng.integers(1, 9, size=300).tolist(), 4, 2, 64, "bf16"),
 ]
 
 
