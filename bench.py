@@ -32,14 +32,16 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def load_traffic(workload: str, decode: bool = False):
-    """HBM bytes per attention launch from committed rocprofv3 counters, if
-    they were taken on the current kernel sources; else None."""
-    from paper_2609_39819_amd.profiling import DECODE_SOURCES, EXTEND_SOURCES, read_traffic, source_sha
-    kind = "decode" if decode else "extend"
+def load_traffic(workload: str, kind: str = "extend"):
+    """HBM bytes per launch of the extend, decode or append kernel from
+    committed rocprofv3 counters, if they were taken on the current kernel
+    sources; else None."""
+    from paper_2609_39819_amd.profiling import APPEND_SOURCES, DECODE_SOURCES, EXTEND_SOURCES, read_traffic, \
+        source_sha
     name = workload if workload.startswith(kind) else f"{kind}_{workload}"
     t = read_traffic(os.path.join(ROOT, "profiles", f"{name}_traffic.md"))
-    if t is None or t[0] != source_sha(DECODE_SOURCES if decode else EXTEND_SOURCES):
+    srcs = {"extend": EXTEND_SOURCES, "decode": DECODE_SOURCES, "append": APPEND_SOURCES}[kind]
+    if t is None or t[0] != source_sha(srcs):
         return None
     return t[1]
 
@@ -406,7 +408,16 @@ def main():
             "peak": PEAK_HBM_GBPS,
             "unit": "GB/s",
             "frac": attn_bytes / (ext_avg * 1e-3) / 1e9 / PEAK_HBM_GBPS,
-            "traffic": load_traffic(w.name, decode=True),
+            "traffic": load_traffic(w.name, "decode"),
+        },
+        # the scatter of the new tokens' K/V (HBM-bound; launch-bound below ~100 MB)
+        "append_roofline": {
+            "bound": "hbm",
+            "achieved": append_bytes / (float(app_ms.mean()) * 1e-3) / 1e9,
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": append_bytes / (float(app_ms.mean()) * 1e-3) / 1e9 / PEAK_HBM_GBPS,
+            "traffic": load_traffic(w.name, "append"),
         },
         "gpu": torch.cuda.get_device_name(dev),
         "gcn_arch": torch.cuda.get_device_properties(dev).gcnArchName,

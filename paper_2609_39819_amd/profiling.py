@@ -32,10 +32,13 @@ EXTEND_SOURCES = ("paper_2609_39819_amd/csrc/kvt_extend.hip", "paper_2609_39819_
                   "paper_2609_39819_amd/csrc/kvt_internal.h")
 DECODE_SOURCES = ("paper_2609_39819_amd/csrc/kvt_decode.hip", "paper_2609_39819_amd/csrc/kvt_device.h",
                   "paper_2609_39819_amd/csrc/kvt_internal.h")
+APPEND_SOURCES = ("paper_2609_39819_amd/csrc/kvt_append.hip", "paper_2609_39819_amd/csrc/kvt_internal.h")
 EXTEND_KERNEL = "extend_fwd_kernel"
 DECODE_KERNEL = "decode_kernel"
+APPEND_KERNEL = "append_kv_kernel"
 COPY_KERNEL = "neg_kernel"
-SOURCES = {EXTEND_KERNEL: EXTEND_SOURCES, DECODE_KERNEL: DECODE_SOURCES}
+SOURCES = {EXTEND_KERNEL: EXTEND_SOURCES, DECODE_KERNEL: DECODE_SOURCES, APPEND_KERNEL: APPEND_SOURCES}
+WHAT = {EXTEND_KERNEL: "extend", DECODE_KERNEL: "decode", APPEND_KERNEL: "append"}
 
 
 def source_sha(paths=EXTEND_SOURCES) -> str:
@@ -109,18 +112,19 @@ def cmd_traffic(args) -> str:
     wc = find(w, COPY_KERNEL)["WRITE_SIZE"] * 1024 / copy_bytes
     fe = find(f, args.kernel)["FETCH_SIZE"] * 1024 / fc
     we = find(w, args.kernel)["WRITE_SIZE"] * 1024 / wc
-    what = "decode" if args.kernel == DECODE_KERNEL else "extend"
+    what = WHAT[args.kernel]
     lines = [
         f"# HBM traffic per {what} launch: {args.title}", "",
         f"Command (FETCH_SIZE pass): `{args.cmd.replace('{C}', 'FETCH_SIZE')}`",
         f"Command (WRITE_SIZE pass): `{args.cmd.replace('{C}', 'WRITE_SIZE')}`", "",
         f"Calibration: a {args.copy_mib} MiB fp32 copy kernel (torch.neg) in the same process reads "
-        f"FETCH_SIZE x{fc:.3f} and WRITE_SIZE x{wc:.3f} of its true bytes; the extend figures are divided by those factors.",
+        f"FETCH_SIZE x{fc:.3f} and WRITE_SIZE x{wc:.3f} of its true bytes; the {what} figures are divided by those factors.",
         "",
         "| quantity | value |", "|---|---|",
         f"| fetch bytes per launch | {fe / 1e6:.1f} MB |",
         f"| write bytes per launch | {we / 1e6:.1f} MB |",
-        f"| algorithmic bytes per launch (K/V once + Q + out) | {args.algorithmic / 1e6:.1f} MB |" if args.algorithmic else "",
+        (f"| algorithmic bytes per launch ({ALGO[what]}) | {args.algorithmic / 1e6:.1f} MB |"
+         if args.algorithmic else ""),
         "",
         f"source_sha256: {source_sha(SOURCES[args.kernel])}",
         f"hbm_bytes_per_launch: {int(fe + we)}",
@@ -128,6 +132,9 @@ def cmd_traffic(args) -> str:
         f"write_bytes_per_launch: {int(we)}",
     ]
     return "\n".join(l for l in lines if l is not None) + "\n"
+
+
+ALGO = {"extend": "K/V once + Q + out", "decode": "K/V once + Q + out", "append": "new K/V read + written"}
 
 
 def cmd_counters(args) -> str:
