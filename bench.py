@@ -7,6 +7,11 @@ pages scattered at random over a 2^20-page pool.  Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
 
+Without --steps the timed region holds 20 steps, or as many as fill about
+0.2 s when 20 steps would take under 0.1 s (short workloads, where one
+launch's latency would otherwise weigh on the wall-clock step time); short
+workloads also warm up for at least 0.1 s, so the clock has settled.
+
 ``--gpus N`` with N > 1 exits: the benchmark measures one GPU only.
 """
 from __future__ import annotations
@@ -224,7 +229,8 @@ def bench_manager(args):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default: 20, more for steps under 5 ms; see above)")
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="react_128k")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -256,6 +262,8 @@ def main():
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported", file=sys.stderr)
         sys.exit(2)
+    if args.manager or args.copy:
+        args.steps = 20 if args.steps is None else args.steps
     if args.manager:
         bench_manager(args)
         return
@@ -343,6 +351,23 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    if args.steps is None:
+        # size the timed region from a short untimed probe of back-to-back steps
+        t0 = time.perf_counter()
+        for _ in range(5):
+            step()
+        torch.cuda.synchronize()
+        est = (time.perf_counter() - t0) / 5
+        args.steps = 20 if 20 * est >= 0.1 else int(min(20000, np.ceil(0.2 / est)))
+        if 20 * est < 0.1:
+            extra = int(np.ceil(0.1 / est))
+            for _ in range(extra):
+                step()
+            args.warmup += 5 + extra
+            torch.cuda.synchronize()
+        else:
+            args.warmup += 5
+        log(f"about {est * 1e3:.3f} ms per step: {args.steps} timed steps after {args.warmup} warm-up steps")
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()

@@ -185,11 +185,19 @@ def test_cascade_specific_checks():
 def test_cascade_workspace_bytes():
     pool = _pool(nb=1 << 20, hkv=8, d=128)
     s = _seqs(P=(8192, 20000), S=(2048, 1000), max_blocks=2048)
-    ws = kvt.lib().kvt_cascade_workspace_bytes(ctypes.byref(pool), ctypes.byref(s.struct), 4096, 96)
+    L = kvt.lib()
+    # the shared pass: one fp32 partial set per key split of the shared part
+    # and of the private parts, merged by the combine kernel
+    ws = L.kvt_cascade_workspace_bytes_ex(ctypes.byref(pool), ctypes.byref(s.struct), 4096,
+                                          kvt.CASCADE_SHARED_PASS, 96)
     rows = 3048 * 96
-    parts = ws // (rows * (128 + 2) * 4)       # key splits of the shared part + of the private parts
+    parts = ws // (rows * (128 + 2) * 4)
     assert parts >= 2 and ws == -(-parts * rows * 128 * 4 // 256) * 256 + parts * rows * 2 * 4
-    assert kvt.lib().kvt_cascade_workspace_bytes(ctypes.byref(pool), ctypes.byref(s.struct), 4100, 96) == 0
+    # this shape runs the plain extend plan by default, with its workspace
+    assert L.kvt_cascade_uses_shared_pass(ctypes.byref(pool), ctypes.byref(s.struct), 4096, 96) == 0
+    assert (L.kvt_cascade_workspace_bytes(ctypes.byref(pool), ctypes.byref(s.struct), 4096, 96)
+            == L.kvt_extend_workspace_bytes(ctypes.byref(pool), ctypes.byref(s.struct), 96))
+    assert L.kvt_cascade_workspace_bytes(ctypes.byref(pool), ctypes.byref(s.struct), 4100, 96) == 0
 
 
 def test_cascade_runs_the_plain_plan_when_its_estimate_loses():
