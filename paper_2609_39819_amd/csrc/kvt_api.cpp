@@ -203,10 +203,13 @@ kvt_status check_shared(const kvt_seqs* seqs, int32_t shared_len) {
 // longest unit's share of its key splits, plus the split partials written
 // and read back when split.  kt[b]: key tiles of sequence b, units[b]: its
 // row tiles x kv-heads.
+constexpr double kMergeLaunchUs = 4.0;
+
 double launch_estimate(const std::vector<int64_t>& units, const std::vector<int64_t>& kt, int nsplit,
                        int64_t rows, const kvt_pool* pool, int cus) {
   // one tile of one workgroup takes about 1.8 us at full load; the partials
-  // move at about 5 bytes per ns (written once, read once by the combine)
+  // move at about 5 bytes per ns (written once, read once by the combine),
+  // and the combine launch itself costs about 4 us
   constexpr double kTileUs = 1.8, kBytesPerUs = 5.0e6;
   double work = 0, longest = 0;
   for (size_t b = 0; b < units.size(); ++b) {
@@ -214,7 +217,7 @@ double launch_estimate(const std::vector<int64_t>& units, const std::vector<int6
     longest = std::max(longest, (double)kt[b]);
   }
   double t = std::max(work / cus, longest / nsplit);
-  if (nsplit > 1) t += 2.0 * (double)part_bytes(pool, nsplit, rows) / kBytesPerUs / kTileUs;
+  if (nsplit > 1) t += (2.0 * (double)part_bytes(pool, nsplit, rows) / kBytesPerUs + kMergeLaunchUs) / kTileUs;
   return t;
 }
 
@@ -259,10 +262,16 @@ ExtendPlan cascade_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shar
   }
   const int64_t rows = T * num_q_heads;
   const double t_plain = launch_estimate(units, kt_full, plain.nsplit, rows, pool, cus);
-  const double t_shared = launch_estimate({(int64_t)row_tiles((int32_t)T, G) * H}, {(shared_len + KT - 1) / KT},
-                                          p.nsplit_shared, 0, pool, cus) +
-                          launch_estimate(units, kt_priv, p.nsplit, 0, pool, cus) +
-                          2.0 * (double)p.ws_bytes / 5.0e6 / 1.8;
+  // the shared and private parts share one launch: the work of both spread
+  // over the CUs, or the longest unit of either, plus the partials of every
+  // split of both parts written and merged
+  const double kt_shared = (double)((shared_len + KT - 1) / KT);
+  double work = (double)row_tiles((int32_t)T, G) * H * kt_shared, longest = kt_shared / p.nsplit_shared;
+  for (int b = 0; b < B; ++b) {
+    work += (double)units[b] * kt_priv[b];
+    longest = std::max(longest, (double)kt_priv[b] / p.nsplit);
+  }
+  const double t_shared = std::max(work / cus, longest) + (2.0 * (double)p.ws_bytes / 5.0e6 + kMergeLaunchUs) / 1.8;
   if (t_shared < t_plain) return p;
   ExtendPlan q = plain;
   q.use_shared = false;
@@ -311,6 +320,11 @@ kvt::ExtendArgs base_args(const kvt_pool* pool, const kvt_seqs* seqs, const void
   a.part_base = 0;
   a.nsplit = plan.nsplit;
   a.total_rows = (int32_t)T;
+  a.second = INT32_MAX;   // one group of sequences
+  a.kbeg2 = 0;
+  a.kend2 = INT32_MAX;
+  a.nsplit2 = 1;
+  a.part_base2 = 0;
   if (plan.nsplit > 1) {
     a.part_o = reinterpret_cast<float*>(workspace);
     a.part_ml = reinterpret_cast<float*>(reinterpret_cast<char*>(workspace) +
@@ -600,44 +614,47 @@ kvt_status kvt_cascade_extend_attention_ex(const kvt_pool* pool, const kvt_seqs*
   kvt::ExtendArgs a = base_args(pool, seqs, q, num_q_heads, scale, out, lse, T, parts, workspace);
   a.direct = 0;
 
-  // shared part: every new token of the batch against keys [0, shared_len),
-  // all of them visible (one virtual sequence whose causal limits start at
-  // shared_len - 1), read through the first sequence's table row, with its
-  // own key splits
+  // One launch for both parts, the shared part's (longer) units first, so
+  // the private parts' units fill the CUs the shared part leaves idle at
+  // its end.  Shared part (sequence 0 of the first launch): every new token
+  // of the batch against keys [0, shared_len), all of them visible (one
+  // virtual sequence whose causal limits start at shared_len - 1), read
+  // through the first sequence's table row, with its own key splits.
+  // Private parts (the second group): each sequence over keys
+  // [shared_len, P_b + i], causal.  Sequences beyond one launch's
+  // descriptors go to further launches of private parts only.
   a.nsplit = plan.nsplit_shared;
   a.part_base = 0;
   a.kbeg = 0;
   a.kend = shared_len;
-  a.nseq = 1;
-  a.seq[0] = kvt::SeqDesc{plan.order[0], shared_len - 1, (int32_t)T, 0};
-  a.unit_begin[0] = 0;
-  a.unit_begin[1] = row_tiles((int32_t)T, G) * plan.nsplit_shared;
-  const int64_t shared_grid = (int64_t)a.unit_begin[1] * pool->num_kv_heads;
-  if (shared_grid > INT32_MAX) return KVT_ERR_INVALID_ARG;
-  hipError_t e = kvt::launch_extend(a, pool->dtype, pool->head_dim, (int)shared_grid, s);
-  if (e != hipSuccess) return device_error(e);
-
-  // private parts: each sequence over keys [shared_len, P_b + i], causal
+  a.kbeg2 = shared_len;
+  a.kend2 = INT32_MAX;
+  a.nsplit2 = plan.nsplit;
+  a.part_base2 = plan.nsplit_shared;
   std::vector<int32_t> row_off(seqs->num_seqs + 1, 0);
   for (int b = 0; b < seqs->num_seqs; ++b) row_off[b + 1] = row_off[b] + seqs->suffix_len[b];
-  a.nsplit = plan.nsplit;
-  a.part_base = plan.nsplit_shared;
-  a.kbeg = shared_len;
-  a.kend = INT32_MAX;
-  for (size_t c0 = 0; c0 < plan.order.size(); c0 += kvt::kSeqsPerLaunch) {
-    const int n = (int)std::min<size_t>(kvt::kSeqsPerLaunch, plan.order.size() - c0);
-    a.nseq = n;
+  size_t c0 = 0;
+  for (bool first = true; first || c0 < plan.order.size(); first = false) {
+    int n = 0;
     int32_t units = 0;
-    for (int i = 0; i < n; ++i) {
-      const int b = plan.order[c0 + i];
-      a.seq[i] = kvt::SeqDesc{b, seqs->prefix_len[b], seqs->suffix_len[b], row_off[b]};
-      a.unit_begin[i] = units;
+    if (first) {
+      a.seq[0] = kvt::SeqDesc{plan.order[0], shared_len - 1, (int32_t)T, 0};
+      a.unit_begin[0] = 0;
+      units = row_tiles((int32_t)T, G) * plan.nsplit_shared;
+      n = 1;
+    }
+    a.second = first ? 1 : 0;
+    for (; n < kvt::kSeqsPerLaunch && c0 < plan.order.size(); ++n, ++c0) {
+      const int b = plan.order[c0];
+      a.seq[n] = kvt::SeqDesc{b, seqs->prefix_len[b], seqs->suffix_len[b], row_off[b]};
+      a.unit_begin[n] = units;
       units += row_tiles(seqs->suffix_len[b], G) * plan.nsplit;
     }
+    a.nseq = n;
     a.unit_begin[n] = units;
     const int64_t grid = (int64_t)units * pool->num_kv_heads;
     if (grid > INT32_MAX) return KVT_ERR_INVALID_ARG;
-    e = kvt::launch_extend(a, pool->dtype, pool->head_dim, (int)grid, s);
+    const hipError_t e = kvt::launch_extend(a, pool->dtype, pool->head_dim, (int)grid, s);
     if (e != hipSuccess) return device_error(e);
   }
   return combine(a, pool, out, lse, T, num_q_heads, nparts, s);

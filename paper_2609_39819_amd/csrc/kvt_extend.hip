@@ -75,26 +75,32 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
   const int si = find_seq(a.unit_begin, a.nseq, unit);
   const SeqDesc sd = a.seq[si];
   const int local = unit - a.unit_begin[si];
+  // key range, splits and partial slots of this sequence's group
+  const bool grp2 = si >= a.second;
+  const int kbeg = grp2 ? a.kbeg2 : a.kbeg;
+  const int kend = grp2 ? a.kend2 : a.kend;
+  const int nsplit = grp2 ? a.nsplit2 : a.nsplit;
+  const int part_base = grp2 ? a.part_base2 : a.part_base;
   const int G = a.group;
   const int rows_seq = sd.suffix * G;
   const int ntile = (rows_seq + kExtTileRows - 1) / kExtTileRows;
-  const int rt = ntile - 1 - local / a.nsplit;   // longest row tile first
-  const int split = local % a.nsplit;
+  const int rt = ntile - 1 - local / nsplit;   // longest row tile first
+  const int split = local % nsplit;
   const int r0 = rt * kExtTileRows;
   const int P = sd.prefix;
-  const int L = min(P + sd.suffix, a.kend);      // positions that can be read
+  const int L = min(P + sd.suffix, kend);      // positions that can be read
   const int nblk = (L + kBlock - 1) / kBlock;
 
   // keys this tile needs: from kbeg up to the last query's own position
   // (or kend); the range is split evenly over the key splits
   const int t_last = min(sd.suffix - 1, (r0 + kExtTileRows - 1) / G);
-  const int kmax = min(P + t_last + 1, a.kend);
+  const int kmax = min(P + t_last + 1, kend);
   const int ntiles_kv = (kmax + KT - 1) / KT;
-  const int jlo = a.kbeg / KT;
-  const int per_split = (ntiles_kv - jlo + a.nsplit - 1) / a.nsplit;
+  const int jlo = kbeg / KT;
+  const int per_split = (ntiles_kv - jlo + nsplit - 1) / nsplit;
   const int j0 = jlo + split * per_split;
   const int j1 = min(ntiles_kv, j0 + per_split);
-  const int lim_min = min(P + r0 / G, a.kend - 1);   // smallest last-visible key of the tile
+  const int lim_min = min(P + r0 / G, kend - 1);   // smallest last-visible key of the tile
 
   // ---- this lane's query rows: block b = rows kExtRowsPerWave*wave + 32*b + l32
   int lim[NB];
@@ -107,7 +113,7 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
     if (!row_valid[b]) r = rows_seq - 1;
     const int t = r / G;
     const int h = g * G + (r - t * G);
-    lim[b] = min(P + t, a.kend - 1);                    // last visible position
+    lim[b] = min(P + t, kend - 1);                    // last visible position
     qrow[b] = (int64_t)(sd.row_off + t) * a.num_q_heads + h;
   }
   bf16x8 qreg[NB][KSTEPS];
@@ -284,8 +290,8 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
             if (half * 32 + 8 * (e >> 2) + (e & 3) > thr) s[b][half][e] = -INFINITY;
       }
     }
-    if (j * KT < a.kbeg) {   // first tile of a range that starts inside it
-      const int thr = a.kbeg - j * KT - 4 * hh;          // keys before kbeg: koff < thr
+    if (j * KT < kbeg) {   // first tile of a range that starts inside it
+      const int thr = kbeg - j * KT - 4 * hh;          // keys before kbeg: koff < thr
 #pragma unroll
       for (int b = 0; b < NB; ++b)
 #pragma unroll
@@ -426,7 +432,7 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
         }
       if (a.lse != nullptr && hh == 0) a.lse[qrow[b]] = (m_ref[b] + __builtin_log2f(l_tot)) * kLn2;
     } else {
-      const int64_t prow = (int64_t)(a.part_base + split) * a.total_rows * a.num_q_heads + qrow[b];
+      const int64_t prow = (int64_t)(part_base + split) * a.total_rows * a.num_q_heads + qrow[b];
       float* op = a.part_o + prow * D;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)

@@ -70,6 +70,12 @@ struct ExtendArgs {
   int32_t nsplit;
   int32_t total_rows;   // T of the whole call
   int32_t nseq;
+  // Extend only: sequences second .. nseq-1 form a second group with their
+  // own key range, key splits and first partial slot (a cascade launch: the
+  // shared part as sequence 0, the private parts after it); second = nseq
+  // when the launch has one group.
+  int32_t second;
+  int32_t kbeg2, kend2, nsplit2, part_base2;
   int32_t unit_begin[kSeqsPerLaunch + 1];  // prefix sums of (row tiles x nsplit), longest first
   SeqDesc seq[kSeqsPerLaunch];
 };
