@@ -13,7 +13,9 @@
 #include <atomic>
 #include <cmath>
 #include <cstring>
+#include <functional>
 #include <numeric>
+#include <queue>
 #include <unordered_set>
 #include <vector>
 
@@ -204,6 +206,10 @@ kvt_status check_shared(const kvt_seqs* seqs, int32_t shared_len) {
 // and read back when split.  kt[b]: key tiles of sequence b, units[b]: its
 // row tiles x kv-heads.
 constexpr double kMergeLaunchUs = 4.0;
+// Fixed cost of one workgroup, in key tiles: its prologue (kernel arguments,
+// block-table entries and the first tile's gather, about 3.3 us) and its
+// epilogue.
+constexpr double kUnitTiles = 2.0;
 
 double launch_estimate(const std::vector<int64_t>& units, const std::vector<int64_t>& kt, int nsplit,
                        int64_t rows, const kvt_pool* pool, int cus) {
@@ -216,9 +222,32 @@ double launch_estimate(const std::vector<int64_t>& units, const std::vector<int6
     work += (double)units[b] * kt[b];
     longest = std::max(longest, (double)kt[b]);
   }
-  double t = std::max(work / cus, longest / nsplit);
+  double t = std::max(work / cus, longest / nsplit) + kUnitTiles;
   if (nsplit > 1) t += (2.0 * (double)part_bytes(pool, nsplit, rows) / kBytesPerUs + kMergeLaunchUs) / kTileUs;
   return t;
+}
+
+// Finish time, in key tiles, of one cascade launch: list scheduling of its
+// units in launch order onto the CUs (each unit to the CU that frees first,
+// as workgroups are dispatched): the shared part's shared_jobs units of
+// len_s tiles first, then each sequence's private units (jobs_p[b] of
+// ceil(kt_p[b] / ns_p) tiles); every unit also pays kUnitTiles.
+double cascade_finish(int64_t shared_jobs, double len_s, const std::vector<int64_t>& jobs_p,
+                      const std::vector<int64_t>& kt_p, int ns_p, int cus) {
+  const int64_t rounds = shared_jobs / cus, rest = shared_jobs % cus;
+  std::priority_queue<double, std::vector<double>, std::greater<double>> free_at;
+  for (int c = 0; c < cus; ++c) free_at.push((double)(c < rest ? rounds + 1 : rounds) * (len_s + kUnitTiles));
+  double span = (double)(rest > 0 ? rounds + 1 : rounds) * (len_s + kUnitTiles);
+  for (size_t b = 0; b < jobs_p.size(); ++b) {
+    const double len = std::ceil((double)kt_p[b] / ns_p) + kUnitTiles;
+    for (int64_t j = 0; j < jobs_p[b] * ns_p; ++j) {
+      const double t = free_at.top() + len;
+      free_at.pop();
+      free_at.push(t);
+      span = std::max(span, t);
+    }
+  }
+  return span;
 }
 
 // Cascade: the split plans of the shared part (one virtual sequence of all T
@@ -244,7 +273,50 @@ ExtendPlan cascade_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shar
   ss.prefix_len = &shared_prefix;
   ss.suffix_len = &all_tokens;
   p.nsplit_shared = make_plan(pool, &ss, num_q_heads, T).nsplit;
-  p.ws_bytes = part_bytes(pool, p.nsplit_shared + p.nsplit, T * num_q_heads);
+
+  const int cus = device_cus();
+  const int64_t rows = T * num_q_heads;
+  std::vector<int64_t> units(B), kt_full(B), kt_priv(B), jobs_p(B);
+  int64_t private_jobs = 0;
+  for (int b = 0; b < B; ++b) {
+    units[b] = (int64_t)row_tiles(seqs->suffix_len[b], G) * H;
+    kt_full[b] = ((int64_t)seqs->prefix_len[b] + seqs->suffix_len[b] + KT - 1) / KT;
+    kt_priv[b] = ((int64_t)priv[b] + seqs->suffix_len[b] + KT - 1) / KT;
+    private_jobs += units[b];
+  }
+  for (int i = 0; i < B; ++i) jobs_p[i] = units[p.order[i]];   // launch order, longest first
+  std::vector<int64_t> kt_p(B);
+  for (int i = 0; i < B; ++i) kt_p[i] = kt_priv[p.order[i]];
+  const int64_t shared_jobs = (int64_t)row_tiles((int32_t)T, G) * H * p.nsplit_shared;
+  const double kt_shared = (double)((shared_len + KT - 1) / KT);
+  const double len_s = std::ceil(kt_shared / p.nsplit_shared);
+  // In one launch the private units can fill what the shared part leaves
+  // idle: when they are few, their split count is the one (of 1, 2, 4, 8,
+  // 16) with the earliest list-scheduled finish plus partial cost.
+  auto partial_cost = [&](int ns_p) {
+    return (2.0 * (double)part_bytes(pool, p.nsplit_shared + ns_p, rows) / 5.0e6 + kMergeLaunchUs) / 1.8;
+  };
+  double t_shared = 0;
+  if (private_jobs <= 4 * (int64_t)cus) {
+    int best = 1;
+    double best_t = cascade_finish(shared_jobs, len_s, jobs_p, kt_p, 1, cus) + partial_cost(1);
+    for (int ns = 2; ns <= kvt::kMaxSplits; ns *= 2) {
+      const double t = cascade_finish(shared_jobs, len_s, jobs_p, kt_p, ns, cus) + partial_cost(ns);
+      if (t < best_t - 1e-9) best = ns, best_t = t;
+    }
+    p.nsplit = best;
+    t_shared = best_t;
+  } else {
+    // many private units: the work of both parts spread over the CUs, or
+    // the longest unit of either
+    double work = (double)shared_jobs * len_s, longest = len_s;
+    for (int b = 0; b < B; ++b) {
+      work += (double)units[b] * kt_priv[b];
+      longest = std::max(longest, (double)kt_priv[b] / p.nsplit);
+    }
+    t_shared = std::max(work / cus, longest) + kUnitTiles + partial_cost(p.nsplit);
+  }
+  p.ws_bytes = part_bytes(pool, p.nsplit_shared + p.nsplit, rows);
   if (mode == KVT_CASCADE_SHARED_PASS) return p;
 
   const ExtendPlan plain = make_plan(pool, seqs, num_q_heads, T);
@@ -253,25 +325,7 @@ ExtendPlan cascade_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shar
     q.use_shared = false;
     return q;
   }
-  const int cus = device_cus();
-  std::vector<int64_t> units(B), kt_full(B), kt_priv(B);
-  for (int b = 0; b < B; ++b) {
-    units[b] = (int64_t)row_tiles(seqs->suffix_len[b], G) * H;
-    kt_full[b] = ((int64_t)seqs->prefix_len[b] + seqs->suffix_len[b] + KT - 1) / KT;
-    kt_priv[b] = ((int64_t)priv[b] + seqs->suffix_len[b] + KT - 1) / KT;
-  }
-  const int64_t rows = T * num_q_heads;
   const double t_plain = launch_estimate(units, kt_full, plain.nsplit, rows, pool, cus);
-  // the shared and private parts share one launch: the work of both spread
-  // over the CUs, or the longest unit of either, plus the partials of every
-  // split of both parts written and merged
-  const double kt_shared = (double)((shared_len + KT - 1) / KT);
-  double work = (double)row_tiles((int32_t)T, G) * H * kt_shared, longest = kt_shared / p.nsplit_shared;
-  for (int b = 0; b < B; ++b) {
-    work += (double)units[b] * kt_priv[b];
-    longest = std::max(longest, (double)kt_priv[b] / p.nsplit);
-  }
-  const double t_shared = std::max(work / cus, longest) + (2.0 * (double)p.ws_bytes / 5.0e6 + kMergeLaunchUs) / 1.8;
   if (t_shared < t_plain) return p;
   ExtendPlan q = plain;
   q.use_shared = false;

@@ -117,7 +117,7 @@ CASC_EDGE = [
     ([40000, 33000], [16, 20], 16384, 8, 8, 128, "bf16"),             # short suffixes: private parts split
 ]
 # the default mode's choice for each shape (the host estimate's)
-CASC_EDGE_AUTO_SHARED = [False, False, False, True, True, True]
+CASC_EDGE_AUTO_SHARED = [True, False, True, True, True, True]
 
 
 @pytest.mark.timeout(300)
@@ -133,10 +133,8 @@ def test_cascade_edge_shapes(case):
     ref_o, ref_l = oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len, w.suffix_len, Hkv, w.scale)
     compare(to_f64(out, dt), ref_o, f"casc_edge{case} out")
     compare(lse.cpu().numpy().astype(np.float64), ref_l, f"casc_edge{case} lse")
-    # the default mode runs the plan it reports, bit for bit: the plain extend
-    # for the smallest shapes (the merge launch would cost more than the
-    # shared keys save), the shared pass where short suffixes meet a long
-    # shared prefix
+    # the default mode runs the plan it reports, bit for bit (here the
+    # plain extend only where one sequence's suffix is long)
     assert uses_shared(w, d, shared) == CASC_EDGE_AUTO_SHARED[case]
     auto = run_cascade(w, d, shared, checked=True)
     same_plan = out if CASC_EDGE_AUTO_SHARED[case] else run_extend(w, d, checked=True)
