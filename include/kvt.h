@@ -171,7 +171,9 @@ kvt_status kvt_extend_attention_noalloc(const kvt_pool* pool, const kvt_seqs* se
  * three steps: every new token of the batch attends over the shared keys
  * [0, shared_len) at once (one pass over the shared pages for the whole
  * batch), each sequence attends over its private keys [shared_len, P_b + i],
- * and the two partial results merge by their log-sum-exp weights.
+ * and the two partial results merge by their log-sum-exp weights.  The
+ * first two steps share one kernel launch (the private parts' work fills
+ * the CUs the shared part leaves idle), the merge is a second launch.
  *
  * shared_len: a positive multiple of 16, at most every prefix_len[b]; the
  * first shared_len/16 block-table entries must be the same pages in every

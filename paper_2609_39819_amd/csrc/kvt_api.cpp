@@ -200,17 +200,18 @@ kvt_status check_shared(const kvt_seqs* seqs, int32_t shared_len) {
   return KVT_OK;
 }
 
-// Estimated time of one extend launch in units of one 64-key tile of one
-// 256-row workgroup: the larger of the work spread over the CUs and the
-// longest unit's share of its key splits, plus the split partials written
-// and read back when split.  kt[b]: key tiles of sequence b, units[b]: its
-// row tiles x kv-heads.
+// Cost of the combine launch that merges split partials, in us.
 constexpr double kMergeLaunchUs = 4.0;
 // Fixed cost of one workgroup, in key tiles: its prologue (kernel arguments,
 // block-table entries and the first tile's gather, about 3.3 us) and its
 // epilogue.
 constexpr double kUnitTiles = 2.0;
 
+// Estimated time of one extend launch in units of one 64-key tile of one
+// 256-row workgroup: the larger of the work spread over the CUs and the
+// longest unit's share of its key splits, plus the split partials written
+// and read back when split.  kt[b]: key tiles of sequence b, units[b]: its
+// row tiles x kv-heads.
 double launch_estimate(const std::vector<int64_t>& units, const std::vector<int64_t>& kt, int nsplit,
                        int64_t rows, const kvt_pool* pool, int cus) {
   // one tile of one workgroup takes about 1.8 us at full load; the partials
