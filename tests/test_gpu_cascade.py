@@ -10,7 +10,8 @@ shared prefix: the shared pass) and force the shared pass on the
 forked-agents workload and on edge shapes (a shared length that is not a
 multiple of the 64-key tile, a sequence whose whole prefix is shared, a
 single sequence, D = 64, fp32 storage, key splits in the private parts),
-which are too small for it to win on its own.
+which are too small for it to win on its own), and check that on the edge
+shapes the default mode gives the bits of the plan it reports.
 """
 import numpy as np
 import pytest
@@ -107,6 +108,7 @@ def test_short_messages_over_a_long_shared_prefix():
     torch.cuda.empty_cache()
 
 
+_casc_rng = np.random.default_rng(77)
 CASC_EDGE = [
     # (prefix lengths, suffix lengths, shared, Hq, Hkv, D, dtype)
     ([200, 500, 96], [40, 300, 7], 48, 12, 1, 128, "bf16"),          # shared not a multiple of 64
@@ -115,9 +117,13 @@ CASC_EDGE = [
     ([3000, 2000, 2500], [64, 65, 63], 1600, 16, 8, 64, "bf16"),      # D = 64
     ([700, 900], [33, 40], 320, 4, 1, 64, "f32"),                     # fp32 storage
     ([40000, 33000], [16, 20], 16384, 8, 8, 128, "bf16"),             # short suffixes: private parts split
+    # 300 sequences: the shared part and 255 private parts in the first
+    # launch, the other 45 private parts in a second
+    ((64 + _casc_rng.integers(0, 400, size=300)).tolist(), _casc_rng.integers(1, 9, size=300).tolist(), 64, 4, 2, 64,
+     "bf16"),
 ]
 # the default mode's choice for each shape (the host estimate's)
-CASC_EDGE_AUTO_SHARED = [True, False, True, True, True, True]
+CASC_EDGE_AUTO_SHARED = [True, False, True, True, True, True, False]
 
 
 @pytest.mark.timeout(300)
@@ -134,7 +140,8 @@ def test_cascade_edge_shapes(case):
     compare(to_f64(out, dt), ref_o, f"casc_edge{case} out")
     compare(lse.cpu().numpy().astype(np.float64), ref_l, f"casc_edge{case} lse")
     # the default mode runs the plan it reports, bit for bit (here the
-    # plain extend only where one sequence's suffix is long)
+    # plain extend where one sequence's suffix is long, and for the 300
+    # sequences, whose work is nearly all private)
     assert uses_shared(w, d, shared) == CASC_EDGE_AUTO_SHARED[case]
     auto = run_cascade(w, d, shared, checked=True)
     same_plan = out if CASC_EDGE_AUTO_SHARED[case] else run_extend(w, d, checked=True)
