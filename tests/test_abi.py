@@ -218,6 +218,23 @@ def test_cascade_runs_the_plain_plan_when_its_estimate_loses():
     assert L.kvt_cascade_uses_shared_pass(ctypes.byref(pool), ctypes.byref(long_.struct), 4100, 96) == -1
 
 
+def test_cascade_splits_short_private_parts_to_fill_the_launch():
+    """16 short messages over a 32K shared prefix: the shared part takes 8
+    key splits (768 workgroups, three full rounds of 256 CUs) and the 128
+    private (row tile, kv-head) units, each under 1024 private keys, take 2
+    splits so that they fill a whole fourth round instead of half of it: 10
+    partial sets in the workspace.  The plain extend's rule (at least 1024
+    keys of the shortest sequence per split) would not split them."""
+    L = kvt.lib()
+    pool = _pool(nb=1 << 20, hkv=8, d=128)
+    s = _seqs(P=[32768 + 37 * i for i in range(16)], S=[16] * 16, max_blocks=2100)
+    ws = L.kvt_cascade_workspace_bytes_ex(ctypes.byref(pool), ctypes.byref(s.struct), 32768,
+                                          kvt.CASCADE_SHARED_PASS, 96)
+    rows = 16 * 16 * 96
+    assert ws == -(-10 * rows * 128 * 4 // 256) * 256 + 10 * rows * 2 * 4
+    assert L.kvt_cascade_uses_shared_pass(ctypes.byref(pool), ctypes.byref(s.struct), 32768, 96) == 1
+
+
 def _copy(pool, ids=FAKE_BT, ids_host=None, n=4, host=FAKE_OUT, direction=0):
     h = None if ids_host is None else np.ascontiguousarray(ids_host, dtype=np.int32).ctypes.data_as(
         ctypes.POINTER(ctypes.c_int32))
