@@ -232,7 +232,9 @@ double launch_estimate(const std::vector<int64_t>& units, const std::vector<int6
 // units in launch order onto the CUs (each unit to the CU that frees first,
 // as workgroups are dispatched): the shared part's shared_jobs units of
 // len_s tiles first, then each sequence's private units (jobs_p[b] of
-// ceil(kt_p[b] / ns_p) tiles); every unit also pays kUnitTiles.
+// ceil(kt_p[b] / ns_p) tiles); every unit also pays kUnitTiles.  Callers
+// pass one kv-head's units and its share of the CUs: the units of the
+// kv-heads alternate, so every kv-head's schedule is the same.
 double cascade_finish(int64_t shared_jobs, double len_s, const std::vector<int64_t>& jobs_p,
                       const std::vector<int64_t>& kt_p, int ns_p, int cus) {
   const int64_t rounds = shared_jobs / cus, rest = shared_jobs % cus;
@@ -277,33 +279,38 @@ ExtendPlan cascade_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shar
 
   const int cus = device_cus();
   const int64_t rows = T * num_q_heads;
-  std::vector<int64_t> units(B), kt_full(B), kt_priv(B), jobs_p(B);
-  int64_t private_jobs = 0;
+  std::vector<int64_t> units(B), kt_full(B), kt_priv(B), jobs_p(B), kt_p(B);
+  int64_t head_jobs = 0;   // private units of one kv-head
   for (int b = 0; b < B; ++b) {
     units[b] = (int64_t)row_tiles(seqs->suffix_len[b], G) * H;
     kt_full[b] = ((int64_t)seqs->prefix_len[b] + seqs->suffix_len[b] + KT - 1) / KT;
     kt_priv[b] = ((int64_t)priv[b] + seqs->suffix_len[b] + KT - 1) / KT;
-    private_jobs += units[b];
+    head_jobs += row_tiles(seqs->suffix_len[b], G);
   }
-  for (int i = 0; i < B; ++i) jobs_p[i] = units[p.order[i]];   // launch order, longest first
-  std::vector<int64_t> kt_p(B);
-  for (int i = 0; i < B; ++i) kt_p[i] = kt_priv[p.order[i]];
+  for (int i = 0; i < B; ++i) {   // launch order, longest first; one kv-head's units
+    jobs_p[i] = row_tiles(seqs->suffix_len[p.order[i]], G);
+    kt_p[i] = kt_priv[p.order[i]];
+  }
+  const int head_cus = std::max(1, cus / H);
   const int64_t shared_jobs = (int64_t)row_tiles((int32_t)T, G) * H * p.nsplit_shared;
   const double kt_shared = (double)((shared_len + KT - 1) / KT);
   const double len_s = std::ceil(kt_shared / p.nsplit_shared);
   // In one launch the private units can fill what the shared part leaves
-  // idle: when they are few, their split count is the one (of 1, 2, 4, 8,
-  // 16) with the earliest list-scheduled finish plus partial cost.
+  // idle: when one kv-head's private units fit one round of its CUs, their
+  // split count is the one (trying 1, 2, 4, 8, 16 until the estimate rises)
+  // with the earliest list-scheduled finish plus partial cost.
   auto partial_cost = [&](int ns_p) {
     return (2.0 * (double)part_bytes(pool, p.nsplit_shared + ns_p, rows) / 5.0e6 + kMergeLaunchUs) / 1.8;
   };
   double t_shared = 0;
-  if (private_jobs <= 4 * (int64_t)cus) {
+  if (head_jobs <= head_cus) {
+    const int64_t head_shared = shared_jobs / H;
     int best = 1;
-    double best_t = cascade_finish(shared_jobs, len_s, jobs_p, kt_p, 1, cus) + partial_cost(1);
+    double best_t = cascade_finish(head_shared, len_s, jobs_p, kt_p, 1, head_cus) + partial_cost(1);
     for (int ns = 2; ns <= kvt::kMaxSplits; ns *= 2) {
-      const double t = cascade_finish(shared_jobs, len_s, jobs_p, kt_p, ns, cus) + partial_cost(ns);
-      if (t < best_t - 1e-9) best = ns, best_t = t;
+      const double t = cascade_finish(head_shared, len_s, jobs_p, kt_p, ns, head_cus) + partial_cost(ns);
+      if (t >= best_t - 1e-9) break;
+      best = ns, best_t = t;
     }
     p.nsplit = best;
     t_shared = best_t;
