@@ -129,6 +129,39 @@ int row_tiles(int32_t suffix, int group) {
   return (int)((rows + kvt::kExtTileRows - 1) / kvt::kExtTileRows);
 }
 
+// Cost of the combine launch that merges split partials, in us.
+constexpr double kMergeLaunchUs = 4.0;
+// Fixed cost of one workgroup, in key tiles: its prologue (kernel arguments,
+// block-table entries and the first tile's gather, about 3.3 us) and its
+// epilogue.
+constexpr double kUnitTiles = 2.0;
+
+// Finish time, in key tiles, of one extend launch: list scheduling of its
+// units in launch order onto the CUs (each unit to the CU that frees first,
+// as workgroups are dispatched): shared_jobs units of len_s tiles first
+// (a cascade's shared part; none for a plain extend), then each sequence's
+// units (jobs_p[b] row tiles of ceil(kt_p[b] / ns_p) tiles, ns_p splits
+// each); every unit also pays kUnitTiles.  Callers pass one kv-head's units
+// and its share of the CUs: the units of the kv-heads alternate, so every
+// kv-head's schedule is the same.
+double list_finish(int64_t shared_jobs, double len_s, const std::vector<int64_t>& jobs_p,
+                      const std::vector<int64_t>& kt_p, int ns_p, int cus) {
+  const int64_t rounds = shared_jobs / cus, rest = shared_jobs % cus;
+  std::priority_queue<double, std::vector<double>, std::greater<double>> free_at;
+  for (int c = 0; c < cus; ++c) free_at.push((double)(c < rest ? rounds + 1 : rounds) * (len_s + kUnitTiles));
+  double span = (double)(rest > 0 ? rounds + 1 : rounds) * (len_s + kUnitTiles);
+  for (size_t b = 0; b < jobs_p.size(); ++b) {
+    const double len = std::ceil((double)kt_p[b] / ns_p) + kUnitTiles;
+    for (int64_t j = 0; j < jobs_p[b] * ns_p; ++j) {
+      const double t = free_at.top() + len;
+      free_at.pop();
+      free_at.push(t);
+      span = std::max(span, t);
+    }
+  }
+  return span;
+}
+
 // Split long key ranges only when the row tiles alone cannot fill the chip.
 ExtendPlan make_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t num_q_heads, int64_t T) {
   ExtendPlan p;
@@ -158,6 +191,37 @@ ExtendPlan make_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t num_q_h
   for (int s = 2; s <= ns_max; ++s)
     if (rounds(s) < rounds(ns) - 1e-9) ns = s;
   if (rounds(ns) > 0.9 * rounds(1)) ns = 1;
+  // Ragged batches: the rule above counts units as equal and keeps 1024 keys
+  // of the shortest sequence per split, so one short sequence stops the long
+  // ones from splitting.  When one kv-head's row tiles fit a few rounds of
+  // its CUs, list-schedule the launch for 1, 2, 4, 8 and 16 splits (one
+  // kv-head's units on its share of the CUs, each unit's length from its
+  // sequence's key tiles) and take the best finish plus partial cost if it
+  // beats the rule's choice by more than a fifth.
+  const int H = pool->num_kv_heads;
+  const int head_cus = std::max(1, cus / H);
+  if (units / H <= 4 * (int64_t)head_cus) {
+    const int64_t rows = T * num_q_heads;
+    std::vector<int64_t> jobs(B), kt(B);
+    for (int i = 0; i < B; ++i) {
+      const int b = p.order[i];
+      jobs[i] = row_tiles(seqs->suffix_len[b], G);
+      kt[i] = ((int64_t)seqs->prefix_len[b] + seqs->suffix_len[b] + kvt::kExtKeysPerTile - 1) / kvt::kExtKeysPerTile;
+    }
+    auto cost = [&](int s) {
+      double t = list_finish(0, 0.0, jobs, kt, s, head_cus);
+      if (s > 1) t += (2.0 * (double)part_bytes(pool, s, rows) / 5.0e6 + kMergeLaunchUs) / 1.8;
+      return t;
+    };
+    const double rule_cost = cost(ns);
+    int best = ns;
+    double best_cost = rule_cost;
+    for (int s = 1; s <= kvt::kMaxSplits; s *= 2) {
+      const double c = cost(s);
+      if (c < best_cost - 1e-9) best = s, best_cost = c;
+    }
+    if (best_cost < 0.8 * rule_cost) ns = best;
+  }
   p.nsplit = ns;
   if (ns > 1) p.ws_bytes = part_bytes(pool, ns, T * num_q_heads);
   return p;
@@ -200,13 +264,6 @@ kvt_status check_shared(const kvt_seqs* seqs, int32_t shared_len) {
   return KVT_OK;
 }
 
-// Cost of the combine launch that merges split partials, in us.
-constexpr double kMergeLaunchUs = 4.0;
-// Fixed cost of one workgroup, in key tiles: its prologue (kernel arguments,
-// block-table entries and the first tile's gather, about 3.3 us) and its
-// epilogue.
-constexpr double kUnitTiles = 2.0;
-
 // Estimated time of one extend launch in units of one 64-key tile of one
 // 256-row workgroup: the larger of the work spread over the CUs and the
 // longest unit's share of its key splits, plus the split partials written
@@ -226,31 +283,6 @@ double launch_estimate(const std::vector<int64_t>& units, const std::vector<int6
   double t = std::max(work / cus, longest / nsplit) + kUnitTiles;
   if (nsplit > 1) t += (2.0 * (double)part_bytes(pool, nsplit, rows) / kBytesPerUs + kMergeLaunchUs) / kTileUs;
   return t;
-}
-
-// Finish time, in key tiles, of one cascade launch: list scheduling of its
-// units in launch order onto the CUs (each unit to the CU that frees first,
-// as workgroups are dispatched): the shared part's shared_jobs units of
-// len_s tiles first, then each sequence's private units (jobs_p[b] of
-// ceil(kt_p[b] / ns_p) tiles); every unit also pays kUnitTiles.  Callers
-// pass one kv-head's units and its share of the CUs: the units of the
-// kv-heads alternate, so every kv-head's schedule is the same.
-double cascade_finish(int64_t shared_jobs, double len_s, const std::vector<int64_t>& jobs_p,
-                      const std::vector<int64_t>& kt_p, int ns_p, int cus) {
-  const int64_t rounds = shared_jobs / cus, rest = shared_jobs % cus;
-  std::priority_queue<double, std::vector<double>, std::greater<double>> free_at;
-  for (int c = 0; c < cus; ++c) free_at.push((double)(c < rest ? rounds + 1 : rounds) * (len_s + kUnitTiles));
-  double span = (double)(rest > 0 ? rounds + 1 : rounds) * (len_s + kUnitTiles);
-  for (size_t b = 0; b < jobs_p.size(); ++b) {
-    const double len = std::ceil((double)kt_p[b] / ns_p) + kUnitTiles;
-    for (int64_t j = 0; j < jobs_p[b] * ns_p; ++j) {
-      const double t = free_at.top() + len;
-      free_at.pop();
-      free_at.push(t);
-      span = std::max(span, t);
-    }
-  }
-  return span;
 }
 
 // Cascade: the split plans of the shared part (one virtual sequence of all T
@@ -306,9 +338,9 @@ ExtendPlan cascade_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t shar
   if (head_jobs <= head_cus) {
     const int64_t head_shared = shared_jobs / H;
     int best = 1;
-    double best_t = cascade_finish(head_shared, len_s, jobs_p, kt_p, 1, head_cus) + partial_cost(1);
+    double best_t = list_finish(head_shared, len_s, jobs_p, kt_p, 1, head_cus) + partial_cost(1);
     for (int ns = 2; ns <= kvt::kMaxSplits; ns *= 2) {
-      const double t = cascade_finish(head_shared, len_s, jobs_p, kt_p, ns, head_cus) + partial_cost(ns);
+      const double t = list_finish(head_shared, len_s, jobs_p, kt_p, ns, head_cus) + partial_cost(ns);
       if (t >= best_t - 1e-9) break;
       best = ns, best_t = t;
     }

@@ -322,7 +322,9 @@ CONFIG_NAMES = ("tiny", "gqa_8k", "react_128k", "forked_agents", "mutation_258k"
 # one decoding step of a batch of 32 agent contexts (one new token each), and
 # of 256 contexts (a serving batch: one launch of 256 sequence descriptors)
 # 16 forked sub-agents each adding a short message over a long shared context
-EXTRA_CONFIG_NAMES = ("react_128k_tp4", "decode_batch", "decode_batch256", "forked_short")
+# 8 agents at different depths of their ReAct loops in one extend call (a
+# ragged batch: contexts log-uniform over 2K..128K, 32..128 new tokens each)
+EXTRA_CONFIG_NAMES = ("react_128k_tp4", "decode_batch", "decode_batch256", "forked_short", "ragged_agents")
 
 
 def config_shapes(name: str) -> dict:
@@ -353,6 +355,9 @@ def config_shapes(name: str) -> dict:
         return dict(seed=8, num_q_heads=96, num_kv_heads=8, head_dim=128, dtype="bf16",
                     num_blocks=1 << 18, num_seqs=16, shared_prefix=32768,
                     private_prefix=(0, 1023), suffix=(16, 16))
+    if name == "ragged_agents":
+        return dict(seed=11, num_q_heads=96, num_kv_heads=8, head_dim=128, dtype="bf16",
+                    num_blocks=1 << 20, num_seqs=8, prefix=(2048, 131072), suffix=(32, 128))
     if name == "mutation_258k":
         return dict(seed=5, num_q_heads=96, num_kv_heads=8, head_dim=128, dtype="bf16",
                     num_blocks=1 << 20, prefix=204800, suffix=57344)
@@ -376,6 +381,12 @@ def make_config(name: str, variant: str = "normal", keep_logical: Optional[bool]
     if name in ("forked_agents", "forked_short"):
         P, S = forked_lengths(rng, c["num_seqs"], c["shared_prefix"], c["private_prefix"], c["suffix"])
         sh_blocks = c["shared_prefix"] // BLOCK_SIZE
+    elif name == "ragged_agents":
+        # context lengths log-uniform over the range, new tokens uniform
+        lo, hi = np.log(c["prefix"][0]), np.log(c["prefix"][1])
+        P = np.round(np.exp(rng.uniform(lo, hi, size=c["num_seqs"]))).astype(np.int64)
+        S = rng.integers(c["suffix"][0], c["suffix"][1], size=c["num_seqs"], endpoint=True)
+        sh_blocks = 0
     elif name in ("decode_batch", "decode_batch256"):
         # reused context lengths uniform over the inclusive range, one new token each
         P = rng.integers(c["prefix"][0], c["prefix"][1], size=c["num_seqs"], endpoint=True)

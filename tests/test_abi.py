@@ -317,6 +317,14 @@ def test_workspace_bytes_follow_the_split_plan():
     # long suffix (2048 x 96 heads): 768 row tiles fill the chip, no split
     s3 = _seqs(P=(131072,), S=(2048,), max_blocks=8320)
     assert _ws_bytes(_pool(nb=1 << 20, hkv=8, d=128), s3, 96) == 0
+    # one GPU's share under 4-way head parallelism: 192 row tiles -> 4 splits
+    assert _ws_bytes(_pool(nb=1 << 20, hkv=2, d=128), s3, 24) == 4 * 2048 * 24 * (128 + 2) * 4
+    # a ragged batch (contexts 1K..32K, 16 new tokens each): the shortest
+    # context alone would allow no split, yet the 32K sequence's row tile
+    # would run alone at the end; list scheduling splits 16 ways
+    s4 = _seqs(P=[1024 * 2 ** i for i in range(6)], S=[16] * 6, max_blocks=2100)
+    rows4 = 6 * 16 * 96
+    assert _ws_bytes(_pool(nb=1 << 20, hkv=8, d=128), s4, 96) == 16 * rows4 * 128 * 4 + 16 * rows4 * 2 * 4
     # invalid arguments -> 0
     assert _ws_bytes(pool, s, 33) == 0
 

@@ -20,9 +20,10 @@ torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
 
 SAMPLE = {"tiny": None, "gqa_8k": None, "react_128k": 48, "forked_agents": 6, "mutation_258k": 16,
-          "react_128k_tp4": 48}
-# the five workloads, plus one GPU's share of the 128K turn under 4-way head parallelism
-ALL = ["tiny", "gqa_8k", "react_128k", "forked_agents", "mutation_258k", "react_128k_tp4"]
+          "react_128k_tp4": 48, "ragged_agents": 12}
+# the five workloads, plus one GPU's share of the 128K turn under 4-way head
+# parallelism and a ragged batch of 8 agent contexts (2K..128K)
+ALL = ["tiny", "gqa_8k", "react_128k", "forked_agents", "mutation_258k", "react_128k_tp4", "ragged_agents"]
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -158,6 +159,31 @@ def test_runs_are_bit_identical_and_split_agrees():
     ref, _ = oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len, w.suffix_len, w.num_kv_heads, w.scale)
     compare(to_f64(c, w.dtype), ref, "gqa_8k unsplit")
     compare(to_f64(a, w.dtype), to_f64(c, w.dtype), "split vs unsplit", max_abs=1e-2, mean_abs=5e-4)
+    del d
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(600)
+def test_ragged_batch_splits_and_agrees():
+    """A ragged batch (contexts 2.3K..97K, 46..127 new tokens): the planner
+    splits the key ranges although the shortest context has few keys (the
+    longest sequence's row tiles would otherwise run alone at the end);
+    split and unsplit agree, and both match the oracle on sampled rows."""
+    from paper_2609_39819_amd import kvt
+    w = cached_config("ragged_agents")
+    d = stage(w)
+    run_append(w, d)
+    need = kvt.extend_workspace_bytes(d["k_pool"], d["v_pool"], d["block_table"], w.prefix_len, w.suffix_len,
+                                      w.num_q_heads)
+    assert need > 0, "the ragged batch runs split"
+    split = run_extend(w, d)
+    whole = run_extend(w, d, use_workspace=False)
+    compare(to_f64(split, w.dtype), to_f64(whole, w.dtype), "ragged split vs unsplit", max_abs=1e-2, mean_abs=5e-4)
+    rows = sample_rows(w, 6, seed=3)
+    kp, vp = oracle_pools("ragged_agents")
+    ref, _ = oracle_extend(w.q, kp, vp, w.compact_table, w.prefix_len, w.suffix_len, w.num_kv_heads, w.scale,
+                           rows=rows)
+    compare(gather_rows(to_f64(whole, w.dtype), w, rows), ref, "ragged unsplit")
     del d
     torch.cuda.empty_cache()
 
