@@ -1,7 +1,8 @@
 """Closed forms checked over every row at full size (no oracle sampling).
 
-The oracle compares sampled rows at the 128K turn, the forked batch and the
-258K mutation; these inputs have answers that need no oracle, so every
+The oracle compares sampled rows at the 128K turn, the forked batch, the
+258K mutation and the ragged agent batch (a split plan over contexts of very
+different lengths); these inputs have answers that need no oracle, so every
 (token, head) row of the output is checked against them:
 
 * needle: each query's target logit is 40 and every other visible logit is
@@ -74,7 +75,7 @@ def _run(name, variant):
 
 
 @pytest.mark.timeout(1200)
-@pytest.mark.parametrize("name", ["react_128k", "forked_agents", "mutation_258k"])
+@pytest.mark.parametrize("name", ["react_128k", "forked_agents", "mutation_258k", "ragged_agents"])
 def test_needle_every_row_returns_its_target_value(name):
     w, got = _run(name, "needle")
     _, vp = oracle_pools(name, "needle")
@@ -97,7 +98,7 @@ def test_needle_every_row_returns_its_target_value(name):
 
 
 @pytest.mark.timeout(1200)
-@pytest.mark.parametrize("name", ["forked_agents", "mutation_258k"])
+@pytest.mark.parametrize("name", ["forked_agents", "mutation_258k", "ragged_agents"])
 def test_zero_keys_every_row_is_its_window_mean(name):
     w, got = _run(name, "kzero")
     _, vp = oracle_pools(name, "kzero")
