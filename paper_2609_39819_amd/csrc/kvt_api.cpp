@@ -145,7 +145,7 @@ constexpr double kUnitTiles = 2.0;
 // and its share of the CUs: the units of the kv-heads alternate, so every
 // kv-head's schedule is the same.
 double list_finish(int64_t shared_jobs, double len_s, const std::vector<int64_t>& jobs_p,
-                      const std::vector<int64_t>& kt_p, int ns_p, int cus) {
+                   const std::vector<int64_t>& kt_p, int ns_p, int cus) {
   const int64_t rounds = shared_jobs / cus, rest = shared_jobs % cus;
   std::priority_queue<double, std::vector<double>, std::greater<double>> free_at;
   for (int c = 0; c < cus; ++c) free_at.push((double)(c < rest ? rounds + 1 : rounds) * (len_s + kUnitTiles));
@@ -173,10 +173,13 @@ ExtendPlan make_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t num_q_h
     return (int64_t)seqs->prefix_len[x] + seqs->suffix_len[x] > (int64_t)seqs->prefix_len[y] + seqs->suffix_len[y];
   });
   int64_t units = 0;
-  int64_t min_keys = INT64_MAX;
+  int64_t min_keys = INT64_MAX, min_len = INT64_MAX, max_len = 0;
   for (int b = 0; b < B; ++b) {
     units += (int64_t)row_tiles(seqs->suffix_len[b], G) * pool->num_kv_heads;
     min_keys = std::min<int64_t>(min_keys, (int64_t)seqs->prefix_len[b] + 1);
+    const int64_t len = (int64_t)seqs->prefix_len[b] + seqs->suffix_len[b];
+    min_len = std::min(min_len, len);
+    max_len = std::max(max_len, len);
   }
   const int cus = device_cus();
   // Split the key range when whole rounds of workgroups over the CUs leave
@@ -193,14 +196,15 @@ ExtendPlan make_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t num_q_h
   if (rounds(ns) > 0.9 * rounds(1)) ns = 1;
   // Ragged batches: the rule above counts units as equal and keeps 1024 keys
   // of the shortest sequence per split, so one short sequence stops the long
-  // ones from splitting.  When one kv-head's row tiles fit a few rounds of
-  // its CUs, list-schedule the launch for 1, 2, 4, 8 and 16 splits (one
-  // kv-head's units on its share of the CUs, each unit's length from its
-  // sequence's key tiles) and take the best finish plus partial cost if it
-  // beats the rule's choice by more than a fifth.
+  // ones from splitting.  When the longest key range is more than twice the
+  // shortest and one kv-head's row tiles fit a few rounds of its CUs,
+  // list-schedule the launch for 1, 2, 4, 8 and 16 splits (one kv-head's
+  // units on its share of the CUs, each unit's length from its sequence's
+  // key tiles) and take the best finish plus partial cost if it beats the
+  // rule's choice by more than a fifth.
   const int H = pool->num_kv_heads;
   const int head_cus = std::max(1, cus / H);
-  if (units / H <= 4 * (int64_t)head_cus) {
+  if (max_len > 2 * min_len && units / H <= 4 * (int64_t)head_cus) {
     const int64_t rows = T * num_q_heads;
     std::vector<int64_t> jobs(B), kt(B);
     for (int i = 0; i < B; ++i) {

@@ -123,7 +123,7 @@ CASC_EDGE = [
      "bf16"),
 ]
 # the default mode's choice for each shape (the host estimate's)
-CASC_EDGE_AUTO_SHARED = [True, False, False, False, False, True, False]
+CASC_EDGE_AUTO_SHARED = [True, False, True, True, True, True, False]
 
 
 @pytest.mark.timeout(300)
