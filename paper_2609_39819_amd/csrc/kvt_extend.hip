@@ -451,28 +451,37 @@ __global__ __launch_bounds__(kThreads) void extend_fwd_kernel(const ExtendArgs a
 
 // Merge the per-split partial results of each row (fixed split order):
 //   m* = max_s m_s,  w_s = 2^(m_s - m*),  out = sum_s w_s O_s / sum_s w_s l_s.
+// One thread per 16 columns of a row: four 16-byte loads per split in flight,
+// and each split's (m, l) read once per 16 columns.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void extend_combine_kernel(const CombineArgs a) {
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // (row, 4-column group)
-  constexpr int Q4 = D / 4;
-  if (idx >= a.rows * Q4) return;
-  const int64_t row = idx / Q4;
-  const int c4 = (int)(idx - row * Q4) * 4;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // (row, 16-column group)
+  constexpr int Q16 = D / 16;
+  if (idx >= a.rows * Q16) return;
+  const int64_t row = idx / Q16;
+  const int c16 = (int)(idx - row * Q16) * 16;
   float mstar = -INFINITY;
   for (int s = 0; s < a.nsplit; ++s) mstar = fmaxf(mstar, a.part_ml[(s * a.rows + row) * 2]);
   float lsum = 0.f;
-  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  f32x4 acc[4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
   for (int s = 0; s < a.nsplit; ++s) {
     const int64_t pr = s * a.rows + row;
     const float m = a.part_ml[pr * 2];
     const float w = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m - mstar);
     lsum += w * a.part_ml[pr * 2 + 1];
-    const f32x4 v = *reinterpret_cast<const f32x4*>(a.part_o + pr * D + c4);
-    acc += w * v;
+    const f32x4* src = reinterpret_cast<const f32x4*>(a.part_o + pr * D + c16);
+    f32x4 v[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) v[k] = src[k];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) acc[k] += w * v[k];
   }
   const float inv = 1.0f / lsum;
-  store4(reinterpret_cast<T*>(a.out) + row * D + c4, acc[0] * inv, acc[1] * inv, acc[2] * inv, acc[3] * inv);
-  if (a.lse != nullptr && c4 == 0) a.lse[row] = (mstar + __builtin_log2f(lsum)) * kLn2;
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+    store4(reinterpret_cast<T*>(a.out) + row * D + c16 + 4 * k, acc[k][0] * inv, acc[k][1] * inv, acc[k][2] * inv,
+           acc[k][3] * inv);
+  if (a.lse != nullptr && c16 == 0) a.lse[row] = (mstar + __builtin_log2f(lsum)) * kLn2;
 }
 
 }  // namespace
@@ -487,7 +496,7 @@ hipError_t launch_extend(const ExtendArgs& a, int dtype, int head_dim, int grid,
 }
 
 hipError_t launch_combine(const CombineArgs& a, int dtype, int head_dim, hipStream_t stream) {
-  const int64_t n = a.rows * (head_dim / 4);
+  const int64_t n = a.rows * (head_dim / 16);
   dim3 g((unsigned)((n + 255) / 256)), b(256);
   if (dtype == 0 && head_dim == 128) hipLaunchKernelGGL((extend_combine_kernel<__bf16, 128>), g, b, 0, stream, a);
   else if (dtype == 0 && head_dim == 64) hipLaunchKernelGGL((extend_combine_kernel<__bf16, 64>), g, b, 0, stream, a);
