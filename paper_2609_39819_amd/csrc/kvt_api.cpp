@@ -141,18 +141,19 @@ constexpr double kUnitTiles = 2.0;
 // as workgroups are dispatched): shared_jobs units of len_s tiles first
 // (a cascade's shared part; none for a plain extend), then each sequence's
 // units (jobs_p[b] row tiles of ceil(kt_p[b] / ns_p) tiles, ns_p splits
-// each); every unit also pays kUnitTiles.  Callers pass one kv-head's units
-// and its share of the CUs: the units of the kv-heads alternate, so every
-// kv-head's schedule is the same.
+// each, of which one in `share` falls to the CUs modelled); every unit also
+// pays kUnitTiles.  Callers model one kv-head's units on its share of the
+// CUs (the units of the kv-heads alternate) or one XCD's (workgroups go to
+// the XCDs in turn).
 double list_finish(int64_t shared_jobs, double len_s, const std::vector<int64_t>& jobs_p,
-                   const std::vector<int64_t>& kt_p, int ns_p, int cus) {
+                   const std::vector<int64_t>& kt_p, int ns_p, int cus, int share = 1) {
   const int64_t rounds = shared_jobs / cus, rest = shared_jobs % cus;
   std::priority_queue<double, std::vector<double>, std::greater<double>> free_at;
   for (int c = 0; c < cus; ++c) free_at.push((double)(c < rest ? rounds + 1 : rounds) * (len_s + kUnitTiles));
   double span = (double)(rest > 0 ? rounds + 1 : rounds) * (len_s + kUnitTiles);
   for (size_t b = 0; b < jobs_p.size(); ++b) {
     const double len = std::ceil((double)kt_p[b] / ns_p) + kUnitTiles;
-    for (int64_t j = 0; j < jobs_p[b] * ns_p; ++j) {
+    for (int64_t j = 0; j < (jobs_p[b] * ns_p + share - 1) / share; ++j) {
       const double t = free_at.top() + len;
       free_at.pop();
       free_at.push(t);
@@ -197,23 +198,23 @@ ExtendPlan make_plan(const kvt_pool* pool, const kvt_seqs* seqs, int32_t num_q_h
   // Ragged batches: the rule above counts units as equal and keeps 1024 keys
   // of the shortest sequence per split, so one short sequence stops the long
   // ones from splitting.  When the longest key range is more than twice the
-  // shortest and one kv-head's row tiles fit a few rounds of its CUs,
-  // list-schedule the launch for 1, 2, 4, 8 and 16 splits (one kv-head's
-  // units on its share of the CUs, each unit's length from its sequence's
-  // key tiles) and take the best finish plus partial cost if it beats the
-  // rule's choice by more than a fifth.
-  const int H = pool->num_kv_heads;
-  const int head_cus = std::max(1, cus / H);
-  if (max_len > 2 * min_len && units / H <= 4 * (int64_t)head_cus) {
+  // shortest and the row tiles fit a few rounds of the CUs, list-schedule
+  // the launch for 1, 2, 4, 8 and 16 splits (one XCD's eighth of the units
+  // on its CUs, each unit's length from its sequence's key tiles) and take
+  // the best finish plus partial cost if it beats the rule's choice by more
+  // than a fifth.
+  constexpr int kXcds = 8;
+  const int xcd_cus = std::max(1, cus / kXcds);
+  if (max_len > 2 * min_len && units <= 4 * (int64_t)cus) {
     const int64_t rows = T * num_q_heads;
     std::vector<int64_t> jobs(B), kt(B);
     for (int i = 0; i < B; ++i) {
       const int b = p.order[i];
-      jobs[i] = row_tiles(seqs->suffix_len[b], G);
+      jobs[i] = (int64_t)row_tiles(seqs->suffix_len[b], G) * pool->num_kv_heads;
       kt[i] = ((int64_t)seqs->prefix_len[b] + seqs->suffix_len[b] + kvt::kExtKeysPerTile - 1) / kvt::kExtKeysPerTile;
     }
     auto cost = [&](int s) {
-      double t = list_finish(0, 0.0, jobs, kt, s, head_cus);
+      double t = list_finish(0, 0.0, jobs, kt, s, xcd_cus, kXcds);
       if (s > 1) t += (2.0 * (double)part_bytes(pool, s, rows) / 5.0e6 + kMergeLaunchUs) / 1.8;
       return t;
     };
