@@ -159,8 +159,11 @@ _I32_MIN, _I32_MAX = -(1 << 31), (1 << 31) - 1
 
 def _i32_array(x) -> ctypes.Array:
     # short lists of Python ints (the common case: a few sequence lengths)
-    # skip numpy; anything else goes through it, which rejects values
-    # outside int32 instead of wrapping them
+    # skip numpy's per-call overhead, and so do short 1-D integer arrays
+    # (turned into such a list first); anything else goes through numpy,
+    # which rejects values outside int32 instead of wrapping them
+    if type(x) is np.ndarray and x.ndim == 1 and x.dtype.kind in "iu" and x.size <= 64:
+        x = x.tolist()
     if type(x) in (list, tuple) and len(x) <= 64 and all(type(e) is int and _I32_MIN <= e <= _I32_MAX for e in x):
         return (ctypes.c_int32 * len(x))(*x)
     a = np.asarray(x)
